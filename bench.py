@@ -1,0 +1,303 @@
+"""Benchmark of one trajectory-verification step on one MI355X.
+
+A step is the whole hot path over one batch of synthetic input already resident in
+HBM: trajectory-masked attention (traj_verify_attn), the confidence/top-k logit pass
+(traj_confidence_topk) and acceptance (traj_accept), launched back to back on one
+stream.  Metric: verified draft tokens per second = B*N*L / step time.
+
+Default workload: "8b-batched" -- 16 sequences, 64 tree-structured drafts of 32
+tokens each (3-ary, levels 3+9+27+25), 32 heads of dim 128, a 4096-token dual
+cache (3584 prefix + 512 suffix), 32768 logit rows over a 126464-token vocabulary.
+Other workloads: --workload 1..5 (see synthetic/workloads.py).
+
+Prints ONE JSON line.  Timing: W warm-up steps, then K timed steps bracketed by
+synchronisation; per-kernel durations come from HIP events recorded on the launch
+stream around every call.  Small workloads rotate several input copies so that the
+reads come from HBM rather than the 256 MB Infinity Cache.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+import paper_2608_27514_amd as tsp  # noqa: E402
+from synthetic import WORKLOADS, attention_inputs, decode_inputs, make_logits, seed_for, torch_dtype  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+MALL_BYTES = 256 << 20
+
+
+def depths(parent_row):
+    out = []
+    for n in range(len(parent_row)):
+        d, j = 1, int(parent_row[n])
+        while j != -1:
+            d += 1
+            j = int(parent_row[j])
+        out.append(d)
+    return out
+
+
+def attn_flops(wl, parent):
+    """Algorithmic FLOP: 4*L*D*(S + L*|anc*(i)|) per (sequence, head, draft)."""
+    tot = 0
+    for b in range(wl.B):
+        for dep in depths(parent[b]):
+            tot += 4 * wl.L * wl.D * (wl.S + wl.L * dep) * wl.Hq
+    return tot
+
+
+def attn_bytes(wl):
+    """Each tensor read or written once: K/V cache, q, out, draft K/V (bf16)."""
+    return 2 * wl.D * wl.B * (2 * wl.S * wl.Hkv + wl.N * wl.L * (2 * wl.Hq + 2 * wl.Hkv))
+
+
+def logit_bytes(wl):
+    elem = 2 if wl.logits_dtype == "bf16" else 4
+    return wl.rows * wl.V * elem + wl.rows * wl.k * 8
+
+
+class StepInputs:
+    def __init__(self, wl, seed, tau, dev):
+        self.wl = wl
+        self.d = decode_inputs(wl, seed, tau=tau)
+        self.q, self.kc, self.vc, self.kd, self.vd = attention_inputs(wl, seed, device=dev)
+        self.parent = torch.as_tensor(self.d["parent"], dtype=torch.int32, device=dev)
+        self.logits = make_logits(self.d["row_margin"], self.d["row_top"], wl.V, torch_dtype(wl.logits_dtype),
+                                  seed + 17, device=dev, row_chunk=2048)
+        self.tokens = torch.as_tensor(self.d["tokens"], device=dev)
+        self.committed = torch.as_tensor(self.d["committed"], device=dev)
+        self.conf0 = torch.as_tensor(self.d["conf0"], device=dev)
+        self.idx0 = torch.as_tensor(self.d["idx0"], device=dev)
+
+    def nbytes(self):
+        ts = [self.q, self.kc, self.vc, self.kd, self.vd, self.logits]
+        return sum(t.numel() * t.element_size() for t in ts)
+
+    def replant(self, seed, tau):
+        """Re-plant tree tokens and logits for another threshold (attention unchanged)."""
+        wl = self.wl
+        dev = self.q.device
+        self.d = decode_inputs(wl, seed, tau=tau, parent=self.d["parent"], rank=self.d["rank"],
+                               level=self.d["level"])
+        make_logits(self.d["row_margin"], self.d["row_top"], wl.V, torch_dtype(wl.logits_dtype), seed + 17,
+                    device=dev, row_chunk=2048, out=self.logits)
+        self.tokens = torch.as_tensor(self.d["tokens"], device=dev)
+        self.committed = torch.as_tensor(self.d["committed"], device=dev)
+        self.conf0 = torch.as_tensor(self.d["conf0"], device=dev)
+        self.idx0 = torch.as_tensor(self.d["idx0"], device=dev)
+
+
+class Buffers:
+    def __init__(self, wl, dev, logits):
+        self.out = torch.empty((wl.B, wl.N, wl.L, wl.Hq, wl.D), dtype=torch.bfloat16, device=dev)
+        self.conf = torch.empty((wl.rows, wl.k), dtype=torch.float32, device=dev)
+        self.idx = torch.empty((wl.rows, wl.k), dtype=torch.int32, device=dev)
+        n = tsp.confidence_topk_workspace_size(logits, wl.k)
+        self.ws = torch.empty(max(n, 16), dtype=torch.uint8, device=dev) if n > 0 else None
+        self.acc = {
+            "leaf": torch.empty(wl.B, dtype=torch.int32, device=dev),
+            "on_path": torch.empty((wl.B, wl.N), dtype=torch.uint8, device=dev),
+            "n_accepted": torch.empty(wl.B, dtype=torch.int32, device=dev),
+            "out_tokens": torch.empty((wl.B, wl.L), dtype=torch.int32, device=dev),
+            "hi": torch.empty((wl.B, wl.N, wl.L), dtype=torch.uint8, device=dev),
+        }
+
+
+def run_step(x, buf, tau, stream, ev=None):
+    if ev is not None:
+        ev[0].record(stream)
+    tsp.verify_attn(x.q, x.kc, x.vc, x.kd, x.vd, x.parent, out=buf.out, stream=stream)
+    if ev is not None:
+        ev[1].record(stream)
+    tsp.confidence_topk(x.logits, x.wl.k, conf=buf.conf, idx=buf.idx, workspace=buf.ws, stream=stream)
+    if ev is not None:
+        ev[2].record(stream)
+    tsp.accept(buf.conf, buf.idx, x.tokens, x.parent, x.committed, x.conf0, x.idx0, tau, out=buf.acc,
+               stream=stream)
+    if ev is not None:
+        ev[3].record(stream)
+
+
+def cpu_baseline(x, buf, wl, tau, n_seq):
+    """The oracle, as it stands, on the first n_seq sequences of the same inputs; also
+    checks the GPU outputs of those sequences against it."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    sl = slice(0, n_seq)
+    f64 = lambda t: t[sl].float().cpu().numpy().astype(np.float64)  # noqa: E731
+    q, kc, vc, kd, vd = (f64(t) for t in (x.q, x.kc, x.vc, x.kd, x.vd))
+    rows = n_seq * wl.N * wl.L
+    lg = x.logits[:rows].float().cpu().numpy()
+    parent = x.d["parent"][sl]
+    t0 = time.perf_counter()
+    ref_out = oracle.verify_attention(q, kc, vc, kd, vd, parent)
+    t1 = time.perf_counter()
+    rc, ri = oracle.confidence_topk(lg, wl.k)
+    t2 = time.perf_counter()
+    shp = (n_seq, wl.N, wl.L, wl.k)
+    ref_acc = oracle.accept_batch(x.d["tokens"][sl], parent, x.d["committed"][sl],
+                                  x.d["conf0"][sl].astype(np.float64), x.d["idx0"][sl], rc.reshape(shp),
+                                  ri.reshape(shp), tau)
+    t3 = time.perf_counter()
+    # sample parity of the timed GPU outputs
+    g_out = buf.out[sl].float().cpu().numpy()
+    attn_ok = bool((np.abs(g_out - ref_out) <= 2e-3 + 2e-2 * np.abs(ref_out)).all())
+    idx_ok = bool(np.array_equal(buf.idx[:rows].cpu().numpy(), ri))
+    conf_err = float(np.abs(buf.conf[:rows].cpu().numpy() - rc).max())
+    leaf_ok = bool(np.array_equal(buf.acc["leaf"][sl].cpu().numpy(), ref_acc["leaf"]))
+    fragile = sum(int(oracle.fragile_states(x.d["tokens"][b], x.d["committed"][b], x.d["conf0"][b],
+                                            rc.reshape(shp)[b], tau).any()) for b in range(n_seq))
+    total = t3 - t0
+    return {
+        "value": rows / total,
+        "unit": "tokens/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": (f"first {n_seq} of {wl.B} sequences ({rows} draft tokens: all {wl.Hq} heads of "
+                   f"attention, {rows} logit rows, acceptance); fp64 numpy, BLAS threads={blas_threads}, "
+                   f"other parts single-threaded"),
+        "seconds": {"attention": t1 - t0, "confidence_topk": t2 - t1, "accept": t3 - t2, "total": total},
+        "sample_parity": {"attention_within_tol": attn_ok, "topk_idx_exact": idx_ok,
+                          "conf_max_abs_err": conf_err, "leaf_exact": leaf_ok,
+                          "fragile_sequences_excluded": fragile},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-seqs", type=int, default=1)
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs the verification step on exactly one GPU; "
+                                   "sequences shard across GPUs with no exchange, so N>1 is N independent "
+                                   "copies of this benchmark and is not launched here"}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+    tsp.load()  # fails loudly when the HIP library is missing
+
+    wl = WORKLOADS[args.workload]
+    tau = wl.tau if args.tau is None else args.tau
+    dev = torch.device("cuda:0")
+    seed = seed_for(wl.cid)
+    x = StepInputs(wl, seed, tau, dev)
+    copies = [x]
+    per_copy = x.nbytes()
+    n_copies = max(1, min(8, math.ceil(2 * MALL_BYTES / per_copy)))
+    for c in range(1, n_copies):
+        copies.append(StepInputs(wl, seed + 101 * c, tau, dev))
+    buf = Buffers(wl, dev, x.logits)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        run_step(copies[i % n_copies], buf, tau, stream)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        run_step(copies[i % n_copies], buf, tau, stream, evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    t_attn = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    t_conf = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    t_acc = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+
+    tokens = wl.B * wl.N * wl.L
+    flops = attn_flops(wl, x.d["parent"])
+    a_tflops = flops / (t_attn * 1e-3) / 1e12
+    l_gbs = logit_bytes(wl) / (t_conf * 1e-3) / 1e9
+    # the last timed step used copies[(K-1) % n]; rerun copy 0 so outputs match x
+    run_step(x, buf, tau, stream)
+    torch.cuda.synchronize()
+    acc_main = buf.acc["n_accepted"].cpu().numpy()
+    status = tsp.device_status(reset=True)
+
+    result = {
+        "metric": "verified draft tokens/sec/GPU",
+        "value": tokens / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; stands in for the paper's benchmarks and LLaDA/Dream activations)",
+        "config": {
+            "workload": f"{wl.name}: B{wl.B} N{wl.N} L{wl.L} Hq{wl.Hq} Hkv{wl.Hkv} D{wl.D} "
+                        f"S{wl.S}({wl.S_prefix}+{wl.S_suffix}) V{wl.V} {wl.logits_dtype} logits, k{wl.k}, "
+                        f"tau {tau}",
+            "draft_tokens_per_step": tokens,
+            "tree": "levels " + "+".join(map(str, wl.level_sizes)) if wl.level_sizes else "explicit parents",
+            "input_copies_rotated": n_copies,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "verify_attn",
+            "achieved": a_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": a_tflops / PEAK_BF16_TFLOPS,
+            "traffic": None,
+            "algorithmic_flop_per_launch": flops,
+        },
+        "kernels_ms": {"verify_attn": t_attn, "confidence_topk": t_conf, "accept": t_acc},
+        "logit_pass": {"bound": "hbm", "achieved": l_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                       "frac": l_gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": logit_bytes(wl)},
+        "attention_hbm_bytes_per_launch": attn_bytes(wl),
+        "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
+        "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},
+        "device_status": status,
+    }
+    if wl.cid == 5 and not args.no_sweep:
+        for t2 in (0.7, 0.8):
+            x.replant(seed, t2)
+            run_step(x, buf, t2, stream)
+            torch.cuda.synchronize()
+            a = buf.acc["n_accepted"].cpu().numpy()
+            result["accepted_tokens_per_step"][str(t2)] = float(a.sum())
+            result["mean_accepted_per_sequence"][str(t2)] = float(a.mean())
+        x.replant(seed, tau)
+        run_step(x, buf, tau, stream)
+        torch.cuda.synchronize()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(x, buf, wl, tau, min(args.cpu_sample_seqs, wl.B))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

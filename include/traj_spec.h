@@ -1,0 +1,192 @@
+/*
+ * traj_spec.h -- C ABI of libtrajspec, the MI355X (gfx950) trajectory-verification step
+ * for trajectory-level speculative decoding of diffusion language models.
+ *
+ * One verification step of the method (Sec. 3.1 overview, stage 3) runs three calls
+ * back to back on one HIP stream:
+ *   1. traj_verify_attn      -- attention of every draft block under the trajectory mask
+ *                               (Sec. 3.3, "Attention masking for trajectory isolation").
+ *   2. traj_confidence_topk  -- per-position confidence c(x) = max softmax and top-k
+ *                               candidates over the vocabulary (Sec. 3.2, Eq. 2 and
+ *                               "Candidate collection").
+ *   3. traj_accept           -- threshold-decoding consistency of every draft with its
+ *                               parent state and the greedy / longest-path walk
+ *                               (Sec. 3.3, "Verification procedure"; Sec. 2.1 threshold
+ *                               decoding; Alg. 1 phase 1 for the high-confidence set).
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
+ *     current when the call is made.  The library never frees or retains them and
+ *     allocates no device memory.
+ *   - Calls validate their host-visible arguments, enqueue kernels on `stream` (a
+ *     hipStream_t passed as void*; NULL = the legacy default stream) and return without
+ *     synchronising.  Results are ready when the stream has reached that point.
+ *   - Errors are returned as traj_status, never thrown.  When a call returns anything but
+ *     TRAJ_OK nothing was enqueued (except TRAJ_E_HIP, which reports a failed launch).
+ *   - Conditions that only the device can see (a parent array that is not topological)
+ *     never cause out-of-bounds accesses: the kernels treat such a parent as -1 and set a
+ *     bit in a per-device status word that traj_get_device_status() reads.
+ *   - bf16 means IEEE-754 binary32 truncated to its upper 16 bits (bfloat16), passed as
+ *     raw 16-bit storage.  Outputs are rounded to nearest even.
+ */
+#ifndef TRAJ_SPEC_H
+#define TRAJ_SPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TRAJ_OK = 0,
+    TRAJ_E_NULL = 1,        /* a required pointer is NULL                              */
+    TRAJ_E_SHAPE = 2,       /* a size is out of range or inconsistent                 */
+    TRAJ_E_DTYPE = 3,       /* unknown element type                                   */
+    TRAJ_E_UNSUPPORTED = 4, /* valid but not implemented here (e.g. head_dim 96)      */
+    TRAJ_E_WORKSPACE = 5,   /* workspace too small or misaligned                      */
+    TRAJ_E_HIP = 6,         /* the HIP runtime reported an error                      */
+    TRAJ_E_ARG = 7          /* an enumerated argument has an unknown value            */
+} traj_status;
+
+typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
+
+/* Device status bits (traj_get_device_status). */
+#define TRAJ_DEV_BAD_PARENT 0x1 /* some parent[n] was outside [-1, n): treated as -1 */
+
+/* ------------------------------------------------------------------------------------
+ * 1. Trajectory-masked verification attention  (Sec. 3.3; drafts packed as in Sec. 3.2
+ *    "Complexity analysis": one concatenated forward over all draft blocks)
+ *
+ * For every sequence b, draft n, block position p and query head h:
+ *     out[b,n,p,h,:] = softmax_j( scale * q[b,n,p,h,:] . key_j ) * value_j
+ * over the keys j VISIBLE to draft n:
+ *     - all S dual-cache tokens k_cache[b,s,g,:] (prefix and suffix; frozen for the block),
+ *     - all L tokens of draft n itself (bidirectional),
+ *     - all L tokens of every ancestor of draft n (draft_parent chain up to -1),
+ * and no token of any other draft.  g = h / (Hq / Hkv) (query heads of one K/V head are
+ * contiguous).  With every parent -1 this is exactly the paper's isolation mask.
+ * The softmax is taken in fp32 with fp32 accumulation; out is rounded to bf16.
+ *
+ * Layouts (row-major, contiguous, bf16):
+ *     q, out            [B, N, L, Hq, D]
+ *     k_cache, v_cache  [B, S, Hkv, D]
+ *     k_draft, v_draft  [B, N, L, Hkv, D]
+ *     draft_parent      [B, N] int32; -1 = child of the committed state, else parent[n] < n
+ * Limits: D in {64, 128}; Hq % Hkv == 0; 1 <= N <= 64; 1 <= L; S >= 0; B >= 1;
+ *         all pointers 16-byte aligned.  RoPE, if any, is already applied by the caller.
+ * scale <= 0 selects 1/sqrt(D).
+ * workspace: optional device scratch (may be NULL with workspace_bytes 0).  When it is at
+ * least traj_verify_attn_workspace_size() bytes the cache keys may be split across more
+ * workgroups for small batches; results are identical up to fp32 summation order.
+ * out must not alias any input.
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    int32_t B, N, L, Hq, Hkv, D, S;
+    float scale;
+} traj_attn_shape;
+
+size_t traj_verify_attn_workspace_size(const traj_attn_shape* shape);
+
+traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                             const void* k_draft, const void* v_draft,
+                             const int32_t* draft_parent, void* out,
+                             const traj_attn_shape* shape,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * 2. Confidence and top-k candidates  (Sec. 3.2, Eq. 2; "Candidate collection")
+ *
+ * For each row r of `logits` (rows x vocab, row r starting at logits + r*row_stride
+ * elements):
+ *     m = max_v l_v,   s = sum_v exp(l_v - m),
+ *     idx[r, 0..k-1]  = the k largest entries, larger first; equal values order by the
+ *                       lower vocabulary index,
+ *     conf[r, j]      = exp(l_idx[r,j] - m) / s          (conf[r,0] is c(x)).
+ * Values are compared as stored (bf16 or fp32), the sum and the quotient are fp32.
+ * Rows must not contain NaN and must hold at least one finite value.
+ * conf: [rows, k] float32, idx: [rows, k] int32 (device).  rows == 0 is a no-op (NULL allowed).
+ * Limits: 1 <= k <= 8; k <= vocab; vocab < 2^31; row_stride >= vocab.
+ * workspace: may be NULL with workspace_bytes 0; with at least
+ * traj_confidence_topk_workspace_size() bytes (16-byte aligned) short batches split each
+ * row across several workgroups and merge the partial results.
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    int64_t rows, vocab, row_stride;
+    int32_t dtype; /* traj_dtype */
+} traj_logits_shape;
+
+size_t traj_confidence_topk_workspace_size(const traj_logits_shape* shape, int32_t k);
+
+traj_status traj_confidence_topk(const void* logits, int32_t k, float* conf, int32_t* idx,
+                                 const traj_logits_shape* shape,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * 3. Acceptance  (Sec. 3.3 "Verification procedure"; Sec. 2.1 threshold decoding;
+ *    Sec. 3.1 logit reuse; Alg. 1 phase 1)
+ *
+ * A block state is an [L] int32 array of token ids with -1 for a masked position.
+ * state(-1) = committed[b] with candidates conf0/idx0 (the previous step's output);
+ * state(n)  = tokens[b,n]  with candidates conf/idx of draft n's rows.
+ * step_tau(s, C, I): if s has no masked position there is no step; otherwise unmask every
+ *   masked p with C[p,0] > threshold (strict) with token I[p,0]; if there is none, unmask
+ *   only the masked p of largest C[p,0] (smallest p on equal values).
+ * Draft c with parent q is consistent when
+ *   TRAJ_MODE_EXACT: tokens[c] == step_tau(state(q)) at every position;
+ *   TRAJ_MODE_TOP1 : it keeps every unmasked token of state(q), unmasks at least one new
+ *                    position, and every new token equals I_q[p,0];
+ *   TRAJ_MODE_TOPK : as TOP1 with the new token among I_q[p,0..k-1].
+ * Traversal TRAJ_GREEDY walks from the committed state, always taking the lowest-index
+ * consistent child; TRAJ_LONGEST takes, among drafts whose whole root path is
+ * consistent, the one unmasking the most committed-masked positions (lowest index on
+ * ties).  Outputs per sequence:
+ *   leaf[b]            accepted draft, -1 if none
+ *   on_path[b,n]       1 if draft n lies on the root path of leaf
+ *   n_accepted[b]      #positions masked in committed[b] and unmasked in the leaf (0 if none)
+ *   out_tokens[b,:]    tokens[b,leaf], or committed[b] when leaf = -1
+ *   hi[b,n,p]          1 if tokens[b,n,p] is masked and conf[b,n,p,0] > threshold
+ * conf/idx are traj_confidence_topk's outputs for rows ordered (b, n, p): [B,N,L,k].
+ * Limits: 1 <= N <= 64; 1 <= L <= 64; 1 <= k <= 8; B >= 1.  All arrays are device arrays.
+ * ------------------------------------------------------------------------------------ */
+enum { TRAJ_MODE_EXACT = 0, TRAJ_MODE_TOP1 = 1, TRAJ_MODE_TOPK = 2 };
+enum { TRAJ_GREEDY = 0, TRAJ_LONGEST = 1 };
+
+typedef struct {
+    int32_t B, N, L, k;
+    const int32_t* tokens;    /* [B,N,L]  -1 = masked                    */
+    const int32_t* parent;    /* [B,N]    -1 = child of committed state  */
+    const int32_t* committed; /* [B,L]    committed block state          */
+    const float* conf0;       /* [B,L,k]  committed state's confidences  */
+    const int32_t* idx0;      /* [B,L,k]  committed state's candidates   */
+    int32_t mode;             /* TRAJ_MODE_*                             */
+    int32_t traversal;        /* TRAJ_GREEDY or TRAJ_LONGEST             */
+} traj_drafts;
+
+typedef struct {
+    int32_t* leaf;       /* [B]      */
+    uint8_t* on_path;    /* [B,N]    */
+    int32_t* n_accepted; /* [B]      */
+    int32_t* out_tokens; /* [B,L]    */
+    uint8_t* hi;         /* [B,N,L]  */
+} traj_accepted;
+
+traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts* drafts,
+                        float threshold, const traj_accepted* accepted, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * Utilities
+ * ------------------------------------------------------------------------------------ */
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* traj_status_string(int32_t status);
+/* Static version string of the library. */
+const char* traj_version(void);
+/* Synchronises `stream`, copies the current device's status word (TRAJ_DEV_* bits) to
+ * *host_flags and, if reset != 0, clears it.  Returns TRAJ_E_HIP on a runtime error. */
+traj_status traj_get_device_status(int32_t* host_flags, int32_t reset, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRAJ_SPEC_H */

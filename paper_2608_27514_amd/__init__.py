@@ -1,0 +1,26 @@
+"""MI355X (gfx950) trajectory-verification step for trajectory-level speculative
+decoding of diffusion language models.
+
+The three calls of one verification step (all HIP kernels in libtrajspec.so):
+
+* :func:`verify_attn`      -- trajectory-masked attention over the dual cache and
+  the packed draft blocks (each draft sees the cache, itself and its ancestors).
+* :func:`confidence_topk`  -- per-position max-softmax confidence and top-k
+  candidates over the vocabulary.
+* :func:`accept`           -- threshold-decoding consistency and greedy /
+  longest-path acceptance of the draft tree.
+"""
+
+from ._lib import (  # noqa: F401
+    DEV_BAD_PARENT,
+    LIB_PATH,
+    TrajSpecError,
+    accept,
+    confidence_topk,
+    confidence_topk_workspace_size,
+    device_status,
+    load,
+    verify_attn,
+    verify_attn_workspace_size,
+    version,
+)

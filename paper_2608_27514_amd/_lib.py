@@ -1,0 +1,229 @@
+"""ctypes binding of libtrajspec (include/traj_spec.h).
+
+Argument marshalling only: every step of the verification path runs in the HIP
+kernels of the library.  PyTorch supplies device memory and the current stream.
+If the library is not built the calls raise -- there is no fallback.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG_DIR, "libtrajspec.so")
+
+TRAJ_OK = 0
+STATUS_NAMES = {0: "TRAJ_OK", 1: "TRAJ_E_NULL", 2: "TRAJ_E_SHAPE", 3: "TRAJ_E_DTYPE",
+                4: "TRAJ_E_UNSUPPORTED", 5: "TRAJ_E_WORKSPACE", 6: "TRAJ_E_HIP", 7: "TRAJ_E_ARG"}
+TRAJ_BF16, TRAJ_F32 = 0, 1
+MODES = {"exact": 0, "top1": 1, "topk": 2}
+TRAVERSALS = {"greedy": 0, "longest": 1}
+DEV_BAD_PARENT = 0x1
+
+
+class TrajSpecError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = _lib().traj_status_string(status).decode()
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({msg})")
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("L", ctypes.c_int32), ("Hq", ctypes.c_int32),
+                ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32), ("S", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class LogitsShape(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("vocab", ctypes.c_int64), ("row_stride", ctypes.c_int64),
+                ("dtype", ctypes.c_int32)]
+
+
+class Drafts(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("L", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("tokens", ctypes.c_void_p), ("parent", ctypes.c_void_p), ("committed", ctypes.c_void_p),
+                ("conf0", ctypes.c_void_p), ("idx0", ctypes.c_void_p), ("mode", ctypes.c_int32),
+                ("traversal", ctypes.c_int32)]
+
+
+class Accepted(ctypes.Structure):
+    _fields_ = [("leaf", ctypes.c_void_p), ("on_path", ctypes.c_void_p), ("n_accepted", ctypes.c_void_p),
+                ("out_tokens", ctypes.c_void_p), ("hi", ctypes.c_void_p)]
+
+
+_LIB = None
+
+EXPORTS = {
+    "traj_verify_attn_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(AttnShape)]),
+    "traj_verify_attn": (ctypes.c_int32, [ctypes.c_void_p] * 7 + [ctypes.POINTER(AttnShape), ctypes.c_void_p,
+                                                                   ctypes.c_size_t, ctypes.c_void_p]),
+    "traj_confidence_topk_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(LogitsShape), ctypes.c_int32]),
+    "traj_confidence_topk": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.POINTER(LogitsShape), ctypes.c_void_p, ctypes.c_size_t,
+                                              ctypes.c_void_p]),
+    "traj_accept": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Drafts), ctypes.c_float,
+                                     ctypes.POINTER(Accepted), ctypes.c_void_p]),
+    "traj_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "traj_version": (ctypes.c_char_p, []),
+    "traj_get_device_status": (ctypes.c_int32, [ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_void_p]),
+}
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_27514_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in EXPORTS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+def load():
+    """Load the library (raises if it is missing) and return its ctypes handle."""
+    return _lib()
+
+
+def version():
+    return _lib().traj_version().decode()
+
+
+def _check(status, where):
+    if status != TRAJ_OK:
+        raise TrajSpecError(status, where)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() > 0 else 0)
+
+
+# ---------------------------------------------------------------- attention
+
+def attn_shape(q, k_cache, scale=0.0):
+    B, N, L, Hq, D = q.shape
+    S, Hkv = k_cache.shape[1], k_cache.shape[2]
+    return AttnShape(B, N, L, Hq, Hkv, D, S, float(scale))
+
+
+def verify_attn_workspace_size(shape):
+    return int(_lib().traj_verify_attn_workspace_size(ctypes.byref(shape)))
+
+
+def verify_attn(q, k_cache, v_cache, k_draft, v_draft, draft_parent, out=None, scale=0.0, workspace=None,
+                stream=None):
+    """Trajectory-masked attention; returns ``out`` [B,N,L,Hq,D] bf16."""
+    for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("k_draft", k_draft),
+                    ("v_draft", v_draft)):
+        _dev(t, name, torch.bfloat16)
+    _dev(draft_parent, "draft_parent", torch.int32)
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", torch.bfloat16)
+    shape = attn_shape(q, k_cache, scale)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib().traj_verify_attn(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_draft), _ptr(v_draft),
+                                 _ptr(draft_parent), _ptr(out), ctypes.byref(shape), _ptr(workspace),
+                                 ws_bytes, _stream(stream))
+    _check(st, "traj_verify_attn")
+    return out
+
+
+# ---------------------------------------------------------------- confidence / top-k
+
+def logits_shape(logits):
+    rows, vocab = logits.shape
+    dt = {torch.bfloat16: TRAJ_BF16, torch.float32: TRAJ_F32}.get(logits.dtype)
+    if dt is None:
+        raise TypeError("logits must be bfloat16 or float32")
+    return LogitsShape(rows, vocab, logits.stride(0), dt)
+
+
+def confidence_topk_workspace_size(logits, k):
+    return int(_lib().traj_confidence_topk_workspace_size(ctypes.byref(logits_shape(logits)), int(k)))
+
+
+def confidence_topk(logits, k, conf=None, idx=None, workspace=None, stream=None):
+    """Returns (conf [R,k] float32, idx [R,k] int32).  ``logits`` [R,V] may have a row
+    stride larger than V (its last dimension must be contiguous)."""
+    if not isinstance(logits, torch.Tensor) or not logits.is_cuda:
+        raise TypeError("logits must be a CUDA (HIP) tensor")
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be 2-D with a contiguous last dimension")
+    shape = logits_shape(logits)
+    R = logits.shape[0]
+    if conf is None:
+        conf = torch.empty((R, k), dtype=torch.float32, device=logits.device)
+    if idx is None:
+        idx = torch.empty((R, k), dtype=torch.int32, device=logits.device)
+    _dev(conf, "conf", torch.float32)
+    _dev(idx, "idx", torch.int32)
+    if workspace is None:
+        need = int(_lib().traj_confidence_topk_workspace_size(ctypes.byref(shape), int(k)))
+        if need > 0:
+            workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib().traj_confidence_topk(ctypes.c_void_p(logits.data_ptr()), int(k), _ptr(conf), _ptr(idx),
+                                     ctypes.byref(shape), _ptr(workspace), ws_bytes, _stream(stream))
+    _check(st, "traj_confidence_topk")
+    return conf, idx
+
+
+# ---------------------------------------------------------------- acceptance
+
+def accept(conf, idx, tokens, parent, committed, conf0, idx0, threshold, mode="exact", traversal="greedy",
+           out=None, stream=None):
+    """Acceptance; returns a dict of device tensors (leaf, on_path, n_accepted,
+    out_tokens, hi).  conf/idx may be [B*N*L, k] or [B,N,L,k]."""
+    B, N, L = tokens.shape
+    k = conf0.shape[-1]
+    if conf.numel() != B * N * L * k or idx.numel() != B * N * L * k:
+        raise ValueError("conf/idx must hold B*N*L*k entries")
+    for name, t, dt in (("conf", conf, torch.float32), ("idx", idx, torch.int32), ("tokens", tokens, torch.int32),
+                        ("parent", parent, torch.int32), ("committed", committed, torch.int32),
+                        ("conf0", conf0, torch.float32), ("idx0", idx0, torch.int32)):
+        _dev(t, name, dt)
+    dev = tokens.device
+    if out is None:
+        out = {
+            "leaf": torch.empty(B, dtype=torch.int32, device=dev),
+            "on_path": torch.empty((B, N), dtype=torch.uint8, device=dev),
+            "n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
+            "out_tokens": torch.empty((B, L), dtype=torch.int32, device=dev),
+            "hi": torch.empty((B, N, L), dtype=torch.uint8, device=dev),
+        }
+    dr = Drafts(B, N, L, k, tokens.data_ptr(), parent.data_ptr(), committed.data_ptr(), conf0.data_ptr(),
+                idx0.data_ptr(), MODES[mode], TRAVERSALS[traversal])
+    ac = Accepted(out["leaf"].data_ptr(), out["on_path"].data_ptr(), out["n_accepted"].data_ptr(),
+                  out["out_tokens"].data_ptr(), out["hi"].data_ptr())
+    st = _lib().traj_accept(_ptr(conf), _ptr(idx), ctypes.byref(dr), float(threshold), ctypes.byref(ac),
+                            _stream(stream))
+    _check(st, "traj_accept")
+    return out
+
+
+def device_status(reset=True, stream=None):
+    """Synchronises the stream and returns the device status bits (TRAJ_DEV_*)."""
+    flags = ctypes.c_int32(0)
+    _check(_lib().traj_get_device_status(ctypes.byref(flags), 1 if reset else 0, _stream(stream)),
+           "traj_get_device_status")
+    return flags.value

@@ -1,0 +1,241 @@
+// libtrajspec: C ABI of the gfx950 trajectory-verification step (see include/traj_spec.h).
+// One translation unit: the kernels live in the headers included below.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/traj_spec.h"
+#include "accept.hpp"
+#include "common.hpp"
+#include "conf_topk.hpp"
+#include "verify_attn.hpp"
+
+namespace {
+
+using namespace trajspec;
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline traj_status launched() { return hipGetLastError() == hipSuccess ? TRAJ_OK : TRAJ_E_HIP; }
+
+// ------------------------------------------------------------------ attention
+traj_status check_attn(const traj_attn_shape* sh) {
+    if (sh->B < 1 || sh->N < 1 || sh->L < 1 || sh->Hq < 1 || sh->Hkv < 1 || sh->S < 0) return TRAJ_E_SHAPE;
+    if (sh->N > 64) return TRAJ_E_SHAPE;
+    if (sh->Hq % sh->Hkv != 0) return TRAJ_E_SHAPE;
+    if (sh->D != 64 && sh->D != 128) return TRAJ_E_UNSUPPORTED;
+    if (!(sh->scale == sh->scale) || std::isinf(sh->scale)) return TRAJ_E_ARG;
+    // flattened element counts must fit the kernels' 64-bit offsets and 32-bit row math
+    const int64_t rows_per_group = (int64_t)(sh->Hq / sh->Hkv) * sh->N * sh->L;
+    if (rows_per_group > (int64_t)1 << 30) return TRAJ_E_SHAPE;
+    if ((int64_t)sh->S * sh->Hkv * sh->D > ((int64_t)1 << 40)) return TRAJ_E_SHAPE;
+    return TRAJ_OK;
+}
+
+template <int D>
+traj_status launch_attn(const AttnParams& p, hipStream_t st) {
+    hipLaunchKernelGGL(verify_attn_kernel<D>, dim3(p.num_wg), dim3(kAttnThreads), 0, st, p);
+    return launched();
+}
+
+// ------------------------------------------------------------------ confidence / top-k
+int vec_of(int32_t dtype) { return dtype == TRAJ_BF16 ? 8 : 4; }
+int size_of(int32_t dtype) { return dtype == TRAJ_BF16 ? 2 : 4; }
+
+traj_status check_logits(const traj_logits_shape* sh, int32_t k) {
+    if (sh->dtype != TRAJ_BF16 && sh->dtype != TRAJ_F32) return TRAJ_E_DTYPE;
+    if (sh->rows < 0 || sh->vocab < 1 || sh->vocab >= ((int64_t)1 << 31)) return TRAJ_E_SHAPE;
+    if (sh->row_stride < sh->vocab) return TRAJ_E_SHAPE;
+    if (sh->rows >= ((int64_t)1 << 31) / 64) return TRAJ_E_SHAPE;
+    if (k < 1 || k > 8 || k > sh->vocab) return TRAJ_E_ARG;
+    return TRAJ_OK;
+}
+
+template <typename T, int K>
+traj_status launch_topk_k(const void* logits, const traj_logits_shape* sh, int k, float* conf, int32_t* idx,
+                          void* ws, size_t ws_bytes, hipStream_t st) {
+    const int vec = VecOf<T>::n;
+    const bool vector_ok = aligned16(logits) && ((sh->row_stride * (int64_t)sizeof(T)) % 16 == 0);
+    TopkPlan plan = plan_conf_topk(sh->rows, sh->vocab, vec);
+    const size_t need = (size_t)sh->rows * plan.splits * kTopkRecord * sizeof(float);
+    if (plan.splits > 1 && (ws == nullptr || ws_bytes < need || !aligned16(ws))) plan = TopkPlan{1, (int)sh->vocab};
+    if (sh->rows == 0) return TRAJ_OK;
+    const int grid = (int)(sh->rows * plan.splits);
+    float* partial = plan.splits > 1 ? static_cast<float*>(ws) : nullptr;
+    const T* lg = static_cast<const T*>(logits);
+    if (vector_ok) {
+        hipLaunchKernelGGL((conf_topk_kernel<T, K, true>), dim3(grid), dim3(kTopkThreads), 0, st, lg,
+                           sh->row_stride, (int)sh->vocab, k, plan.splits, plan.chunk, conf, idx, partial);
+    } else {
+        hipLaunchKernelGGL((conf_topk_kernel<T, K, false>), dim3(grid), dim3(kTopkThreads), 0, st, lg,
+                           sh->row_stride, (int)sh->vocab, k, plan.splits, plan.chunk, conf, idx, partial);
+    }
+    if (plan.splits > 1) {
+        hipLaunchKernelGGL((conf_topk_merge_kernel<K>), dim3((unsigned)sh->rows), dim3(64), 0, st, partial,
+                           (int)sh->rows, plan.splits, k, conf, idx);
+    }
+    return launched();
+}
+
+template <typename T>
+traj_status launch_topk(const void* logits, const traj_logits_shape* sh, int k, float* conf, int32_t* idx,
+                        void* ws, size_t ws_bytes, hipStream_t st) {
+    switch (k) {
+        case 1: return launch_topk_k<T, 1>(logits, sh, k, conf, idx, ws, ws_bytes, st);
+        case 2: return launch_topk_k<T, 2>(logits, sh, k, conf, idx, ws, ws_bytes, st);
+        case 3:
+        case 4: return launch_topk_k<T, 4>(logits, sh, k, conf, idx, ws, ws_bytes, st);
+        default: return launch_topk_k<T, 8>(logits, sh, k, conf, idx, ws, ws_bytes, st);
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t traj_verify_attn_workspace_size(const traj_attn_shape* shape) {
+    (void)shape;
+    return 0;  // the attention kernels need no scratch memory at present
+}
+
+traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_cache, const void* k_draft,
+                             const void* v_draft, const int32_t* draft_parent, void* out,
+                             const traj_attn_shape* shape, void* workspace, size_t workspace_bytes, void* stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    if (shape == nullptr || q == nullptr || k_draft == nullptr || v_draft == nullptr || draft_parent == nullptr ||
+        out == nullptr)
+        return TRAJ_E_NULL;
+    if (shape->S > 0 && (k_cache == nullptr || v_cache == nullptr)) return TRAJ_E_NULL;
+    traj_status st = check_attn(shape);
+    if (st != TRAJ_OK) return st;
+    if (!aligned16(q) || !aligned16(k_draft) || !aligned16(v_draft) || !aligned16(out) ||
+        (shape->S > 0 && (!aligned16(k_cache) || !aligned16(v_cache))))
+        return TRAJ_E_SHAPE;
+
+    AttnParams p{};
+    p.q = static_cast<const uint16_t*>(q);
+    p.kc = static_cast<const uint16_t*>(k_cache);
+    p.vc = static_cast<const uint16_t*>(v_cache);
+    p.kd = static_cast<const uint16_t*>(k_draft);
+    p.vd = static_cast<const uint16_t*>(v_draft);
+    p.parent = draft_parent;
+    p.out = static_cast<uint16_t*>(out);
+    p.B = shape->B;
+    p.N = shape->N;
+    p.L = shape->L;
+    p.Hq = shape->Hq;
+    p.Hkv = shape->Hkv;
+    p.S = shape->S;
+    p.group = shape->Hq / shape->Hkv;
+    p.rows_per_group = p.group * p.N * p.L;
+    const int rb = (p.rows_per_group + 31) / 32;
+    p.wg_per_group = (rb + kAttnWaves - 1) / kAttnWaves;
+    const int64_t nwg = (int64_t)p.B * p.Hkv * p.wg_per_group;
+    if (nwg > 0x7fffffff) return TRAJ_E_SHAPE;
+    p.num_wg = (int)nwg;
+    const float scale = shape->scale > 0.f ? shape->scale : 1.0f / std::sqrt((float)shape->D);
+    p.scale_log2 = scale * 1.4426950408889634f;
+    hipStream_t s = as_stream(stream);
+    return shape->D == 128 ? launch_attn<128>(p, s) : launch_attn<64>(p, s);
+}
+
+size_t traj_confidence_topk_workspace_size(const traj_logits_shape* shape, int32_t k) {
+    if (shape == nullptr || check_logits(shape, k) != TRAJ_OK) return 0;
+    const TopkPlan plan = plan_conf_topk(shape->rows, shape->vocab, vec_of(shape->dtype));
+    if (plan.splits <= 1) return 0;
+    return (size_t)shape->rows * plan.splits * kTopkRecord * sizeof(float);
+}
+
+traj_status traj_confidence_topk(const void* logits, int32_t k, float* conf, int32_t* idx,
+                                 const traj_logits_shape* shape, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+    if (shape == nullptr) return TRAJ_E_NULL;
+    traj_status st = check_logits(shape, k);
+    if (st != TRAJ_OK) return st;
+    if (shape->rows == 0) return TRAJ_OK;  // nothing to do; pointers may be NULL
+    if (logits == nullptr || conf == nullptr || idx == nullptr) return TRAJ_E_NULL;
+    if (workspace != nullptr && !aligned16(workspace)) return TRAJ_E_WORKSPACE;
+    const size_t need = traj_confidence_topk_workspace_size(shape, k);
+    if (workspace != nullptr && workspace_bytes > 0 && workspace_bytes < need) return TRAJ_E_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    if (shape->dtype == TRAJ_BF16) return launch_topk<uint16_t>(logits, shape, k, conf, idx, workspace, workspace_bytes, s);
+    return launch_topk<float>(logits, shape, k, conf, idx, workspace, workspace_bytes, s);
+}
+
+traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts* drafts, float threshold,
+                        const traj_accepted* accepted, void* stream) {
+    if (drafts == nullptr || accepted == nullptr || conf == nullptr || idx == nullptr) return TRAJ_E_NULL;
+    if (drafts->tokens == nullptr || drafts->parent == nullptr || drafts->committed == nullptr ||
+        drafts->conf0 == nullptr || drafts->idx0 == nullptr)
+        return TRAJ_E_NULL;
+    if (accepted->leaf == nullptr || accepted->on_path == nullptr || accepted->n_accepted == nullptr ||
+        accepted->out_tokens == nullptr || accepted->hi == nullptr)
+        return TRAJ_E_NULL;
+    if (drafts->B < 1 || drafts->N < 1 || drafts->N > kMaxDrafts || drafts->L < 1 || drafts->L > kMaxBlock)
+        return TRAJ_E_SHAPE;
+    if (drafts->k < 1 || drafts->k > 8) return TRAJ_E_ARG;
+    if (drafts->mode < TRAJ_MODE_EXACT || drafts->mode > TRAJ_MODE_TOPK) return TRAJ_E_ARG;
+    if (drafts->traversal != TRAJ_GREEDY && drafts->traversal != TRAJ_LONGEST) return TRAJ_E_ARG;
+    if (!(threshold == threshold)) return TRAJ_E_ARG;
+    AcceptParams p{};
+    p.conf = conf;
+    p.idx = idx;
+    p.tokens = drafts->tokens;
+    p.parent = drafts->parent;
+    p.committed = drafts->committed;
+    p.conf0 = drafts->conf0;
+    p.idx0 = drafts->idx0;
+    p.leaf = accepted->leaf;
+    p.on_path = accepted->on_path;
+    p.n_accepted = accepted->n_accepted;
+    p.out_tokens = accepted->out_tokens;
+    p.hi = accepted->hi;
+    p.B = drafts->B;
+    p.N = drafts->N;
+    p.L = drafts->L;
+    p.k = drafts->k;
+    p.mode = drafts->mode;
+    p.traversal = drafts->traversal;
+    p.tau = threshold;
+    hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(kAcceptThreads), 0, as_stream(stream), p);
+    return launched();
+}
+
+const char* traj_status_string(int32_t status) {
+    switch (status) {
+        case TRAJ_OK: return "ok";
+        case TRAJ_E_NULL: return "a required pointer is NULL";
+        case TRAJ_E_SHAPE: return "a size is out of range, inconsistent or misaligned";
+        case TRAJ_E_DTYPE: return "unknown element type";
+        case TRAJ_E_UNSUPPORTED: return "supported by the ABI but not implemented (head_dim must be 64 or 128)";
+        case TRAJ_E_WORKSPACE: return "workspace too small or misaligned";
+        case TRAJ_E_HIP: return "HIP runtime error";
+        case TRAJ_E_ARG: return "an enumerated or scalar argument has an invalid value";
+        default: return "unknown status";
+    }
+}
+
+const char* traj_version(void) { return "libtrajspec 0.1.0 gfx950"; }
+
+traj_status traj_get_device_status(int32_t* host_flags, int32_t reset, void* stream) {
+    if (host_flags == nullptr) return TRAJ_E_NULL;
+    hipStream_t s = as_stream(stream);
+    if (hipStreamSynchronize(s) != hipSuccess) return TRAJ_E_HIP;
+    int32_t v = 0;
+    if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_device_status), sizeof(v), 0, hipMemcpyDeviceToHost) != hipSuccess)
+        return TRAJ_E_HIP;
+    *host_flags = v;
+    if (reset) {
+        const int32_t zero = 0;
+        if (hipMemcpyToSymbol(HIP_SYMBOL(g_device_status), &zero, sizeof(zero), 0, hipMemcpyHostToDevice) !=
+            hipSuccess)
+            return TRAJ_E_HIP;
+    }
+    return TRAJ_OK;
+}
+
+}  // extern "C"

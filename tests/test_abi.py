@@ -1,0 +1,128 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects invalid
+arguments before touching the device (CPU only: no compute calls)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_27514_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "traj_spec.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(_lib.LIB_PATH), reason="libtrajspec.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(traj_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for fn in ("traj_verify_attn", "traj_confidence_topk", "traj_accept"):
+        assert fn in names
+
+
+@needs_lib
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(declared_functions()) == set(_lib.EXPORTS)
+
+
+@needs_lib
+def test_status_strings_and_version():
+    lib = _lib.load()
+    assert lib.traj_version().decode().startswith("libtrajspec")
+    for st in range(8):
+        assert lib.traj_status_string(st)
+    assert lib.traj_status_string(1234) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+@needs_lib
+def test_attention_argument_errors():
+    lib = _lib.load()
+    good = _lib.AttnShape(1, 4, 8, 4, 4, 64, 192, 0.0)
+
+    def call(shape, ptrs=None):
+        p = ptrs or [FAKE] * 7
+        return lib.traj_verify_attn(*p, ctypes.byref(shape), None, 0, None)
+
+    assert call(good, [None] + [FAKE] * 6) == 1
+    assert call(good, [FAKE] * 6 + [None]) == 1
+    assert call(_lib.AttnShape(1, 4, 8, 4, 3, 64, 192, 0.0)) == 2    # Hq % Hkv
+    assert call(_lib.AttnShape(1, 65, 8, 4, 4, 64, 192, 0.0)) == 2   # N > 64
+    assert call(_lib.AttnShape(1, 4, 0, 4, 4, 64, 192, 0.0)) == 2    # L = 0
+    assert call(_lib.AttnShape(1, 4, 8, 4, 4, 96, 192, 0.0)) == 4    # head dim
+    assert call(_lib.AttnShape(1, 4, 8, 4, 4, 64, 192, float("nan"))) == 7
+    mis = [ctypes.c_void_p(0x1002)] + [FAKE] * 6
+    assert call(good, mis) == 2                                       # misaligned q
+    assert lib.traj_verify_attn(*([FAKE] * 7), None, None, 0, None) == 1
+    assert lib.traj_verify_attn_workspace_size(ctypes.byref(good)) == 0
+
+
+@needs_lib
+def test_logits_argument_errors():
+    lib = _lib.load()
+
+    def call(shape, k, logits=FAKE, ws=None, ws_bytes=0):
+        return lib.traj_confidence_topk(logits, k, FAKE, FAKE, ctypes.byref(shape), ws, ws_bytes, None)
+
+    good = _lib.LogitsShape(256, 126464, 126464, 0)
+    assert call(_lib.LogitsShape(4, 100, 100, 9), 3) == 3            # dtype
+    assert call(_lib.LogitsShape(4, 100, 99, 0), 3) == 2             # stride < vocab
+    assert call(good, 0) == 7 and call(good, 9) == 7                  # k range
+    assert call(_lib.LogitsShape(4, 2, 2, 1), 3) == 7                 # k > vocab
+    assert call(good, 3, logits=None) == 1
+    need = lib.traj_confidence_topk_workspace_size(ctypes.byref(good), 3)
+    assert need > 0
+    assert call(good, 3, ws=FAKE, ws_bytes=need - 1) == 5             # too small
+    assert call(good, 3, ws=ctypes.c_void_p(0x1004), ws_bytes=need) == 5  # misaligned
+    big = _lib.LogitsShape(32768, 126464, 126464, 0)
+    assert lib.traj_confidence_topk_workspace_size(ctypes.byref(big), 3) == 0
+
+
+@needs_lib
+def test_accept_argument_errors():
+    lib = _lib.load()
+    f = 0x1000
+    acc = _lib.Accepted(f, f, f, f, f)
+
+    def call(dr, conf=FAKE, tau=0.9, ac=acc):
+        return lib.traj_accept(conf, FAKE, ctypes.byref(dr), tau, ctypes.byref(ac), None)
+
+    good = dict(B=1, N=4, L=8, k=3, tokens=f, parent=f, committed=f, conf0=f, idx0=f, mode=0, traversal=0)
+    assert call(_lib.Drafts(**good), conf=None) == 1
+    assert call(_lib.Drafts(**{**good, "tokens": None})) == 1
+    assert call(_lib.Drafts(**good), ac=_lib.Accepted(f, f, f, f, 0)) == 1
+    assert call(_lib.Drafts(**{**good, "N": 65})) == 2
+    assert call(_lib.Drafts(**{**good, "L": 65})) == 2
+    assert call(_lib.Drafts(**{**good, "k": 9})) == 7
+    assert call(_lib.Drafts(**{**good, "mode": 3})) == 7
+    assert call(_lib.Drafts(**{**good, "traversal": 2})) == 7
+    assert call(_lib.Drafts(**good), tau=float("nan")) == 7
+
+
+def test_product_path_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2608_27514_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in text and "from oracle" not in text, fn
+                assert "oracle/" not in text, fn
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(_lib, "_LIB", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        _lib.load()

@@ -1,0 +1,130 @@
+"""GPU parity: traj_confidence_topk against the fp64 oracle.
+
+conf within 1e-4 absolute; idx bit-exact (equal values rank the lower index).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_27514_amd as tsp
+from synthetic import WORKLOADS, decode_inputs, make_logits, seed_for, torch_dtype
+from helpers import CONF_ATOL
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(logits_gpu, k, rows=None, label=""):
+    conf, idx = tsp.confidence_topk(logits_gpu, k)
+    torch.cuda.synchronize()
+    if rows is None:
+        rows = np.arange(logits_gpu.shape[0])
+    host = logits_gpu[torch.as_tensor(rows, device=logits_gpu.device)].float().cpu().numpy()
+    rc, ri = oracle.confidence_topk(host, k)
+    gc = conf.cpu().numpy()[rows]
+    gi = idx.cpu().numpy()[rows]
+    assert np.array_equal(gi, ri), f"{label}: idx mismatch in {int((gi != ri).any(axis=1).sum())} rows"
+    err = np.abs(gc - rc).max()
+    assert err <= CONF_ATOL, f"{label}: conf err {err}"
+    return conf, idx
+
+
+def test_tiny_fp32_full():
+    wl = WORKLOADS[1]
+    d = decode_inputs(wl, seed_for(1))
+    lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.float32, seed_for(1)).cuda()
+    _check(lg, wl.k, label="tiny-fp32")
+
+
+def test_8b_siblings_full_size():
+    """256 rows x 126464 bf16 -- the launch splits rows (short batch path)."""
+    wl = WORKLOADS[2]
+    d = decode_inputs(wl, seed_for(2))
+    lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(2)).cuda()
+    assert tsp.confidence_topk_workspace_size(lg, 3) > 0
+    _check(lg, 3, label="8b-siblings")
+
+
+@pytest.mark.parametrize("cid", [3, 4])
+def test_full_size_sampled_rows(cid):
+    wl = WORKLOADS[cid]
+    d = decode_inputs(wl, seed_for(cid))
+    lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(cid), device="cuda")
+    rows = np.random.default_rng(cid).choice(lg.shape[0], size=96, replace=False)
+    rows = np.concatenate([[0, lg.shape[0] - 1], rows])
+    _check(lg, 3, rows=rows, label=wl.name)
+
+
+def test_batched_full_size_sampled_rows():
+    wl = WORKLOADS[5]
+    d = decode_inputs(wl, seed_for(5))
+    lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(5), device="cuda",
+                     row_chunk=2048)
+    rows = np.random.default_rng(5).choice(lg.shape[0], size=64, replace=False)
+    rows = np.concatenate([[0, lg.shape[0] - 1], rows])
+    _check(lg, 3, rows=rows, label=wl.name)
+    del lg
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 8])
+def test_exact_ties_every_k(k):
+    rows, V = 300, 5000
+    lg = make_logits(np.zeros(rows), np.zeros((rows, 3), dtype=np.int64), V, torch.bfloat16, 77 + k,
+                     mode="ties").cuda()
+    _check(lg, k, label=f"ties k={k}")
+
+
+def test_raw_margin_rows_and_few_rows_split():
+    wl = WORKLOADS[2].with_(N=1, parents=(-1,))
+    d = decode_inputs(wl, 5)
+    for rows in (1, 3, 32):
+        lg = make_logits(d["row_margin"][:rows], d["row_top"][:rows], wl.V, torch.bfloat16, 9, mode="raw").cuda()
+        _check(lg, 3, label=f"raw rows={rows}")
+
+
+def test_strided_and_unaligned_rows_use_scalar_path():
+    rows, V = 64, 3001
+    base = make_logits(np.zeros(rows), np.zeros((rows, 3), dtype=np.int64), V + 67, torch.bfloat16, 4,
+                       mode="ties").cuda()
+    strided = base[:, :V]              # row stride 3068 elements (16-byte aligned)
+    _check(strided, 3, label="strided")
+    unaligned = base[:, 1:V + 1]       # base pointer off by 2 bytes
+    _check(unaligned, 4, label="unaligned")
+    f32 = make_logits(np.zeros(rows), np.zeros((rows, 3), dtype=np.int64), V + 5, torch.float32, 5,
+                      mode="ties").cuda()[:, 1:V + 1]
+    _check(f32, 2, label="fp32 unaligned")
+
+
+@pytest.mark.parametrize("V", [1, 7, 255, 1000, 2049])
+def test_small_and_ragged_vocab(V):
+    rng = np.random.default_rng(V)
+    x = torch.from_numpy(rng.standard_normal((40, V)).astype(np.float32))
+    for dt in (torch.float32, torch.bfloat16):
+        _check(x.to(dt).cuda(), min(3, V), label=f"V={V} {dt}")
+
+
+def test_negative_infinity_entries():
+    x = torch.full((4, 300), -float("inf"))
+    x[:, 5] = 1.0
+    x[1, 7] = 1.0
+    x[2, 299] = 3.0
+    x[3, :] = torch.linspace(-3, 3, 300)
+    x[3, ::2] = -float("inf")
+    _check(x.cuda(), 3, label="-inf fp32")
+    _check(x.to(torch.bfloat16).cuda(), 3, label="-inf bf16")
+
+
+def test_zero_rows_is_a_no_op():
+    x = torch.empty((0, 100), dtype=torch.bfloat16, device="cuda")
+    conf, idx = tsp.confidence_topk(x, 3)
+    assert conf.shape == (0, 3)
+
+
+def test_bad_arguments_raise():
+    x = torch.zeros((2, 5), dtype=torch.float32, device="cuda")
+    with pytest.raises(tsp.TrajSpecError):
+        tsp.confidence_topk(x, 9)
+    with pytest.raises(tsp.TrajSpecError):
+        tsp.confidence_topk(x, 6)
