@@ -108,8 +108,12 @@ __device__ __forceinline__ void wave_merge(float& m, float& s, TopList<K>& tl) {
 }
 
 // Running update with one vector of NV values starting at vocabulary index id0.
+// `floor_bits` is a lower bound (order_bits form) on the row's k-th largest value shared by
+// the wave: values below it can never reach the row's top-k, so only vectors holding a
+// value >= max(floor, this lane's K-th) take the insertion path.
 template <int K, int NV>
-__device__ __forceinline__ void absorb(const float (&x)[NV], int id0, float& m, float& s, TopList<K>& tl) {
+__device__ __forceinline__ void absorb(const float (&x)[NV], int id0, float& m, float& s, TopList<K>& tl,
+                                       uint32_t floor_bits) {
     float vmax = x[0];
 #pragma unroll
     for (int j = 1; j < NV; ++j) vmax = fmaxf(vmax, x[j]);
@@ -122,10 +126,33 @@ __device__ __forceinline__ void absorb(const float (&x)[NV], int id0, float& m, 
 #pragma unroll
     for (int j = 0; j < NV; ++j) acc += fast_exp2(__builtin_fmaf(x[j], kLog2e, -mL));
     s += acc;
-    if (order_bits(vmax) >= (uint32_t)(tl.key[K - 1] >> 32)) {
+    const uint32_t lane_floor = (uint32_t)(tl.key[K - 1] >> 32);
+    const uint32_t thr = floor_bits > lane_floor ? floor_bits : lane_floor;
+    if (order_bits(vmax) >= thr) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j) tl.insert(make_key(x[j], id0 + j));
+        for (int j = 0; j < NV; ++j) {
+            const uint64_t key = make_key(x[j], id0 + j);
+            if (key > tl.key[K - 1]) tl.insert(key);
+        }
     }
+}
+
+// Lower bound on the k-th largest value of a row from the lanes' running maxima: the k-th
+// largest lane maximum (all copies of each round's maximum are dropped, which can only
+// lower the bound).  Returned in order_bits form; 0 when fewer than k lanes hold a value.
+__device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
+    uint32_t cur = lane_max == kNegInf ? 0u : order_bits(lane_max);
+    uint32_t best = 0;
+    for (int r = 0; r < k; ++r) {
+        best = cur;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const uint32_t o = __shfl_xor(best, off);
+            best = o > best ? o : best;
+        }
+        if (cur == best) cur = 0u;
+    }
+    return best;
 }
 
 // Elements of type T per 16-byte vector.
@@ -170,10 +197,12 @@ __global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
     tl.clear();
 
     int scalar_from = begin;
+    uint32_t floor_bits = 0;
     if (VECTOR) {
         const int nvec = (end - begin) / NV;
         const u32x4_t* vp = reinterpret_cast<const u32x4_t*>(base + begin);
-        for (int vb = 0; vb < nvec; vb += kTopkThreads * kTopkUnroll) {
+        int it = 0;
+        for (int vb = 0; vb < nvec; vb += kTopkThreads * kTopkUnroll, ++it) {
             u32x4_t buf[kTopkUnroll];
 #pragma unroll
             for (int u = 0; u < kTopkUnroll; ++u) {
@@ -186,15 +215,17 @@ __global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
                 if (vi < nvec) {
                     float x[NV];
                     unpack(buf[u], x);
-                    absorb<K, NV>(x, begin + vi * NV, m, s, tl);
+                    absorb<K, NV>(x, begin + vi * NV, m, s, tl, floor_bits);
                 }
             }
+            // refresh the wave floor after iterations 0, 1, 3, 7, 15, ...
+            if ((it & (it + 1)) == 0) floor_bits = wave_kth_floor(m, k);
         }
         scalar_from = begin + nvec * NV;
     }
     for (int e = scalar_from + tid; e < end; e += kTopkThreads) {
         float x[1] = {load_scalar(base + e)};
-        absorb<K, 1>(x, e, m, s, tl);
+        absorb<K, 1>(x, e, m, s, tl, floor_bits);
     }
 
     // lanes -> wave

@@ -180,3 +180,16 @@ def test_bad_shapes_raise():
     with pytest.raises(tsp.TrajSpecError):  # head_dim 96 unsupported
         tsp.verify_attn(q[..., :48].contiguous(), kc[..., :48].contiguous(), vc[..., :48].contiguous(),
                         kd[..., :48].contiguous(), vd[..., :48].contiguous(), par)
+
+
+@pytest.mark.parametrize("S", [1, 63, 64, 65, 127, 128, 129, 191, 192, 193, 255, 256, 257, 320, 383, 384, 449])
+def test_cache_lengths_cover_every_tail_path(S):
+    """The cache loop runs full tiles in pairs and peels 0-2 full tiles plus a last
+    (ragged or full) tile: every cache length class in 64-key tiles must agree."""
+    wl = Workload(98, "cache-len", B=1, N=3, L=32, Hq=2, Hkv=1, D=128, S_prefix=S, S_suffix=0, V=64,
+                  logits_dtype="f32", margin_max=3.0, parents=(-1, 0, 0), level_sizes=None)
+    parent = np.array([[-1, 0, 0]], dtype=np.int32)
+    for variant in ("spec", "sharp"):
+        inputs, _, out = _run(wl, 1000 + S, variant, parent=parent)
+        ok, worst, frac = _check(out, inputs, parent, variant)
+        assert ok, f"S={S} {variant}: worst excess {worst:.3g}, {frac:.2%} bad"
