@@ -36,6 +36,35 @@ from synthetic import WORKLOADS, attention_inputs, decode_inputs, make_logits, s
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 MALL_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {
+    "verify_attn": ("common.hpp", "verify_attn.hpp"),
+    "confidence_topk": ("common.hpp", "conf_topk.hpp"),
+}
+
+
+def kernel_source_hash(kernel):
+    """sha256 over the sources a kernel is built from (traffic figures are only valid for
+    the exact code they were measured on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for fn in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2608_27514_amd", "csrc", fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE passes, or
+    None when they are missing or were taken on different kernel code."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)[kernel][workload]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    return rec["bytes_per_launch"]
 
 
 def depths(parent_row):
@@ -189,7 +218,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seqs", type=int, default=1)
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run three 1 GiB device-to-device copies (for scaling rocprofv3 FETCH_SIZE / "
+                         "WRITE_SIZE readings) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        src = torch.ones((1 << 30) // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 1 << 30, "copy_bytes_written": 1 << 30, "copies": 3}))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this build runs the verification step on exactly one GPU; "
@@ -272,12 +312,13 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": a_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic("verify_attn", wl.name),
             "algorithmic_flop_per_launch": flops,
         },
         "kernels_ms": {"verify_attn": t_attn, "confidence_topk": t_conf, "accept": t_acc},
         "logit_pass": {"bound": "hbm", "achieved": l_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                       "frac": l_gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": logit_bytes(wl)},
+                       "frac": l_gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": logit_bytes(wl),
+                       "traffic": measured_traffic("confidence_topk", wl.name)},
         "attention_hbm_bytes_per_launch": attn_bytes(wl),
         "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
         "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},
