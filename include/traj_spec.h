@@ -75,6 +75,7 @@ typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
  *     k_draft, v_draft  [B, N, L, Hkv, D]
  *     draft_parent      [B, N] int32; -1 = child of the committed state, else parent[n] < n
  * Limits: D in {64, 128}; Hq % Hkv == 0; 1 <= N <= 64; 1 <= L; S >= 0; B >= 1;
+ *         one sequence's cache slice S*Hkv*D*2 bytes below 2 GiB (else TRAJ_E_UNSUPPORTED);
  *         all pointers 16-byte aligned.  RoPE, if any, is already applied by the caller.
  * scale <= 0 selects 1/sqrt(D).
  * workspace: optional device scratch (may be NULL with workspace_bytes 0).  When it is at

@@ -32,6 +32,8 @@ traj_status check_attn(const traj_attn_shape* sh) {
     const int64_t rows_per_group = (int64_t)(sh->Hq / sh->Hkv) * sh->N * sh->L;
     if (rows_per_group > (int64_t)1 << 30) return TRAJ_E_SHAPE;
     if ((int64_t)sh->S * sh->Hkv * sh->D > ((int64_t)1 << 40)) return TRAJ_E_SHAPE;
+    // one sequence's cache slice is addressed through 32-bit buffer offsets
+    if ((int64_t)sh->S * sh->Hkv * sh->D * 2 >= ((int64_t)1 << 31)) return TRAJ_E_UNSUPPORTED;
     return TRAJ_OK;
 }
 
@@ -211,7 +213,7 @@ const char* traj_status_string(int32_t status) {
         case TRAJ_E_NULL: return "a required pointer is NULL";
         case TRAJ_E_SHAPE: return "a size is out of range, inconsistent or misaligned";
         case TRAJ_E_DTYPE: return "unknown element type";
-        case TRAJ_E_UNSUPPORTED: return "supported by the ABI but not implemented (head_dim must be 64 or 128)";
+        case TRAJ_E_UNSUPPORTED: return "supported by the ABI but not implemented (head_dim must be 64 or 128; one sequence's cache below 2 GiB)";
         case TRAJ_E_WORKSPACE: return "workspace too small or misaligned";
         case TRAJ_E_HIP: return "HIP runtime error";
         case TRAJ_E_ARG: return "an enumerated or scalar argument has an invalid value";

@@ -20,19 +20,28 @@
 //   V tile: chunk c of row r is stored at c ^ v_rot(r) (a per-row multiple of 4), so the
 //           4 rows x 64 bytes that half a wave reads with one transposing load cover all
 //           64 banks once.
-//   Tiles are filled with global_load_lds_dwordx4 (16 bytes per lane straight into LDS, no
-//   VGPR staging): each wave-wide load fills one contiguous kilobyte, i.e. whole rows, and
-//   each lane fetches the global chunk that the swizzle puts in its slot.
+//   Cache tiles are filled with buffer_load_dwordx4 ... lds (16 bytes per lane straight into
+//   LDS, no VGPR staging; the (b, g) slice is a buffer descriptor, the uniform row offset
+//   rides in soffset and each lane keeps a 32-bit offset): each wave-wide load fills one
+//   contiguous kilobyte, i.e. whole rows, and each lane fetches the global chunk that the
+//   swizzle puts in its slot.  Draft tiles use global_load_lds_dwordx4 the same way.
 //
 // Phases per workgroup
-//   1. cache: tiles of 64 keys in two LDS buffers (separate arrays, so the compiler can see
-//      that the direct loads into one never alias reads of the other); the next tile's
-//      loads are issued before the current tile is computed, one barrier per tile.  The
-//      loop runs full tiles in pairs with no conditional code and peels the ragged tail.
-//   2. drafts: each wave walks the 32-key tiles of the packed draft keys and processes
-//      only tiles holding its own block or an ancestor block (a 64-bit ancestor mask per
-//      draft, built from the parent array).  Tiles that hold only fully visible blocks need
-//      no per-element mask (always the case when L is a multiple of 32).
+//   0. prologue: the parent array, Q, the K rows of cache block 0 and the first stage are all
+//      requested before anything waits; wave 0 builds the 64-bit ancestor masks from the
+//      parent array with lane shuffles.
+//   1. cache, software-pipelined per 32-key block: the body of block j issues the score
+//      chain of block j+1 on the matrix cores, computes block j's weights on the vector
+//      ALUs in between, then O += V_j P_j.  Stage t holds the K rows of blocks 2t+1, 2t+2 and
+//      the V rows of blocks 2t, 2t+1 in one of two LDS buffers (separate arrays, so the
+//      compiler can see that the direct loads into one never alias reads of the other);
+//      the next stage is loaded while the current one is computed, one barrier per stage.
+//      Stage pairs whose successors are full run with no conditional code; the last stages
+//      take per-block checks for the partial block.
+//   2. drafts: each wave visits only the 32-key tiles holding its own block or an ancestor
+//      block (the set bits of the OR of its rows' ancestor masks, lowest first).  Tiles
+//      that hold only fully visible blocks need no per-element mask (always the case when
+//      L is a multiple of 32 and a wave's rows share a draft).
 #pragma once
 
 #include "common.hpp"
@@ -56,6 +65,8 @@ struct AttnParams {
 };
 
 constexpr int kAttnWaves = 4;
+// Word 3 of a raw (untyped) buffer descriptor on gfx950: 32-bit data format, no swizzle.
+constexpr int kBufferFlags = 0x00020000;
 // s_waitcnt immediate (gfx9 encoding) waiting for vector-memory loads only: vmcnt = 0,
 // expcnt and lgkmcnt left at their maxima.
 constexpr int kWaitVmcnt0 = 0x0F70;
@@ -124,32 +135,52 @@ __device__ __forceinline__ float pair_sum(float x) {
     return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
-// Online-softmax update with one 32-key block of raw scores (masked keys = -inf); the lane
-// holds 16 scores for its query column, lane^32 the other 16.  `m` is the query's reference
-// maximum in raw score units and `c` = scale * log2(e), so a weight is exp2(c * (score - m)):
-// one FMA and one exp2 per score.  The reference only moves (and O and the running sum are
-// only rescaled) when a block maximum exceeds it by more than kLazyLog2 in the log2 domain:
+// Online softmax over 32-key blocks of raw scores (masked keys = -inf).  The lane holds 16
+// scores for its query column, lane^32 the other 16.  `m` is the query's reference maximum in
+// raw score units and `c` = scale * log2(e), so a weight is exp2(c * (score - m)): one FMA and
+// one exp2 per score.  The reference only moves (and O and the running sum are only
+// rescaled) when a block maximum exceeds it by more than kLazyLog2 in the log2 domain:
 // weights then stay below 2^kLazyLog2, which fp32 accumulators and bf16 weights hold at full
 // relative precision, and most blocks skip the rescale.  The decision is per query, the
-// branch wave-uniform.  pf[half] receives the bf16 weights of keys 16*half .. +15 of the
-// block in MFMA B-operand order.
+// branch wave-uniform.
+//
+// Online-softmax state of one query: reference m (raw score units), -c*m (0 while m = -inf),
+// m + thr (the lazy-rescale trigger) and the running sum of weights.  The derived values
+// change only when m moves.
+struct SoftState {
+    float m, neg_mc, mthr, lsum;
+};
+
+// block_max_update: fold the block maximum into `m`, rescaling o and lsum when it moves.
+// Scores are never NaN (finite inputs, -inf for masked keys), so the NaN-propagating
+// maximum (v_maximum3_f32, no operand canonicalisation) is exact here.  `thr` is
+// kLazyLog2 / c in raw score units; with m = -inf the test holds exactly when the block has
+// a visible key.
+
 template <int D>
-__device__ __forceinline__ void softmax_update(const f32x16_t& s, float c, float& m, float& lsum,
-                                               f32x16_t (&o)[D / 32], bf16x8_t (&pf)[2]) {
-    float mx = fmaxf(s[0], s[1]);
+__device__ __forceinline__ void block_max_update(const f32x16_t& s, float c, float thr, SoftState& st,
+                                                 f32x16_t (&o)[D / 32]) {
+    float mx = __builtin_elementwise_maximum(s[0], s[1]);
 #pragma unroll
-    for (int v = 2; v < 16; v += 2) mx = fmaxf(fmaxf(mx, s[v]), s[v + 1]);
+    for (int v = 2; v < 16; v += 2) mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, s[v]), s[v + 1]);
     mx = pair_max(mx);
-    const bool need = (mx - m) * c > kLazyLog2;  // false for an all-masked block (NaN or -inf)
+    const bool need = mx > st.mthr;
     if (ballot64(need) != 0ull) {
-        const float m_new = need ? mx : m;
-        const float alpha = need ? fast_exp2((m - m_new) * c) : 1.0f;  // 0 when m was -inf
-        lsum *= alpha;
+        const float m_new = need ? mx : st.m;
+        const float alpha = need ? fast_exp2((st.m - m_new) * c) : 1.0f;  // 0 when m was -inf
+        st.lsum *= alpha;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
-        m = m_new;
+        st.m = m_new;
+        st.neg_mc = m_new == kNegInf ? 0.f : -m_new * c;
+        st.mthr = m_new + thr;
     }
-    const float neg_mc = m == kNegInf ? 0.f : -m * c;
+}
+
+// block_exp: weights of one block against the current reference (neg_mc = -c*m); pf[half]
+// receives the bf16 weights of keys 16*half .. +15 in MFMA B-operand order, and lsum grows by
+// their fp32 sum.
+__device__ __forceinline__ void block_exp(const f32x16_t& s, float c, float neg_mc, float& lsum, bf16x8_t (&pf)[2]) {
     float sum = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -158,6 +189,22 @@ __device__ __forceinline__ void softmax_update(const f32x16_t& s, float c, float
         pf[v >> 3][v & 7] = (__bf16)p;
     }
     lsum += sum;
+}
+
+template <int D>
+__device__ __forceinline__ void softmax_update(const f32x16_t& s, float c, float thr, SoftState& st,
+                                               f32x16_t (&o)[D / 32], bf16x8_t (&pf)[2]) {
+    block_max_update<D>(s, c, thr, st, o);
+    block_exp(s, c, st.neg_mc, st.lsum, pf);
+}
+
+// Scores of keys key0 .. key0+31 at or beyond S are masked (branch-free select).
+__device__ __forceinline__ void mask_tail(f32x16_t& s, int key0, int S, int h) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int key = key0 + 8 * (v >> 2) + 4 * h + (v & 3);
+        s[v] = key < S ? s[v] : kNegInf;
+    }
 }
 
 // S^T of one 32-key block: kbase = K region + block row offset; kq[ks] = this lane's
@@ -200,74 +247,163 @@ struct AttnLane {
     int pc;           // LDS chunk slot of this lane within that row
 };
 
-// Issue the direct loads of cache tile `tile` into `stage`: wave `wave` (uniform) fills
-// rows [16 wave, 16 wave + 16) of the K and V tiles, kRowsPerDma rows per load.  The
-// global row of each load is uniform, so addresses are a scalar base plus this lane's
-// 32-bit offset.  RAGGED clamps rows >= S to row S-1 (their scores are masked; the
-// clamped values stay finite).
-template <int D, bool RAGGED>
-__device__ __forceinline__ void cache_dma(const uint16_t* kc_base, const uint16_t* vc_base, int kv_stride,
-                                          int tile, int S, int wave, const AttnLane<D>& ln, uint16_t* stage) {
+// Direct loads of 64 cache rows, keys key0 .. key0+63, into the LDS tile `dst` with the
+// chunk swizzle SWZ: wave `wave` (uniform) fills tile rows [16 wave, 16 wave + 16),
+// kRowsPerDma rows per load.  The first global row of each load is uniform, so addresses are
+// a scalar base plus this lane's 32-bit offset.  RAGGED clamps keys >= S to key S-1 (their
+// scores are masked or never computed; the clamped values stay finite); the uniform base row
+// is clamped too, so a lane's offset from it is never negative.
+template <int D, bool RAGGED, bool IS_V>
+__device__ __forceinline__ void cache_rows_dma(__amdgpu_buffer_rsrc_t rs, int kv_stride, int key0, int S, int wave,
+                                               const AttnLane<D>& ln, uint16_t* dst) {
     using G = AttnGeom<D>;
 #pragma unroll
     for (int j = 0; j < G::kDmaPerWave; ++j) {
         const int row0 = wave * (kAttnTile / kAttnWaves) + j * G::kRowsPerDma;  // uniform
         const int r = row0 + ln.ri;                                               // tile row
-        // first global row of this load (uniform) and this lane's row relative to it; in a
-        // ragged tile both are clamped to the last key, so the offset is never negative
-        int base_row = tile * kAttnTile + row0;
+        int base_row = key0 + row0;
         int grow = ln.ri;
         if (RAGGED) {
             base_row = min(base_row, S - 1);
-            grow = min(tile * kAttnTile + r, S - 1) - base_row;
+            grow = min(key0 + r, S - 1) - base_row;
         }
-        const int64_t rowbase = (int64_t)base_row * kv_stride;  // uniform
-        const unsigned ok = (unsigned)(grow * kv_stride + ((ln.pc ^ G::k_swz(r)) << 3));
-        const unsigned ov = (unsigned)(grow * kv_stride + ((ln.pc ^ G::v_rot(r)) << 3));
-        dma16(kc_base + rowbase + ok, stage + row0 * D);
-        dma16(vc_base + rowbase + ov, stage + G::kTileElems + row0 * D);
+        const int swz = IS_V ? G::v_rot(r) : G::k_swz(r);
+        const unsigned voff = 2u * (unsigned)(grow * kv_stride + ((ln.pc ^ swz) << 3));  // lane bytes
+        const unsigned soff = 2u * (unsigned)(base_row * kv_stride);                     // uniform bytes
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + row0 * D), 16, voff, soff, 0, 0);
     }
 }
 
-// One 64-key cache tile from `stage`, one 32-key block at a time.
+// Stage t of the cache pipeline holds the K rows of keys 64 t + 32 .. 64 t + 95 (blocks 2t+1
+// and 2t+2) and the V rows of keys 64 t .. 64 t + 63 (blocks 2t and 2t+1): block j's body
+// multiplies V of block j and computes the scores of block j+1, so both bodies of a stage
+// read one buffer and a single barrier per stage suffices.  RAGGED when 64 t + 96 > S.
 template <int D, bool RAGGED>
-__device__ __forceinline__ void cache_tile(const uint16_t* stage, const AttnLane<D>& ln,
-                                           const bf16x8_t (&qf)[D / 16], float c, int key0, int S, int h,
-                                           float& m, float& lsum, f32x16_t (&o)[D / 32]) {
+__device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t vrs, int kv_stride, int t,
+                                          int S, int wave, const AttnLane<D>& ln, uint16_t* stage) {
     using G = AttnGeom<D>;
+    cache_rows_dma<D, RAGGED, false>(krs, kv_stride, t * kAttnTile + 32, S, wave, ln, stage);
+    cache_rows_dma<D, RAGGED, true>(vrs, kv_stride, t * kAttnTile, S, wave, ln, stage + G::kTileElems);
+}
+
+// K fragments of cache keys 0..31 straight from global memory (the first block of the
+// pipeline, needed before any stage is in LDS), and S^T of a block from such fragments; keys
+// >= S read key S-1 and are masked by the caller.
+template <int D>
+__device__ __forceinline__ void load_k_global(const uint16_t* kc_base, int kv_stride, int S, int lane,
+                                              bf16x8_t (&kf)[D / 16]) {
+    const int key = min(lane & 31, S - 1);
+    const uint16_t* p = kc_base + (int64_t)key * kv_stride + 8 * (lane >> 5);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-        f32x16_t s = qk_block<D>(stage + kb * 32 * D, ln.kq, qf);
-        if (RAGGED) {
+    for (int ks = 0; ks < D / 16; ++ks) kf[ks] = __builtin_bit_cast(bf16x8_t, ldg16(p + 16 * ks));
+}
+
+template <int D>
+__device__ __forceinline__ f32x16_t qk_frags(const bf16x8_t (&kf)[D / 16], const bf16x8_t (&qf)[D / 16]) {
+    f32x16_t s = {};
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int key = key0 + kb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-                s[v] = key < S ? s[v] : kNegInf;
+    for (int ks = 0; ks < D / 16; ++ks) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], s, 0, 0, 0);
+    return s;
+}
+
+// Body of cache block j, software-pipelined: `s` holds the scores of block j (its maximum
+// already folded into m).  The scores of block j+1 (K rows at kn) are issued on the matrix
+// cores, block j's weights are computed on the vector ALUs between the links of that chain,
+// then O += V_j P_j (V rows at vj); finally block j+1's maximum is folded in and `s` becomes
+// block j+1.
+template <int D, bool HAS_NEXT, bool MASK_NEXT>
+__device__ __forceinline__ void cache_body(const uint16_t* kn, const uint16_t* vj, const AttnLane<D>& ln,
+                                           const bf16x8_t (&qf)[D / 16], float c, float thr, int key_next, int S,
+                                           int h, f32x16_t& s, SoftState& st, f32x16_t (&o)[D / 32]) {
+    // A wave issues in order and an MFMA waits for the matrix core, so the body is written in
+    // the order it should issue: the links of the scores chain of block j+1 alternate with the
+    // weights of block j (PER scores per link) and, once the first half of the weights is
+    // ready, with the first half of O += V_j P_j.  Fragment reads run a few links ahead.
+    // sched_barrier(0) keeps the compiler from regrouping (hoisting every read raises register
+    // pressure beyond the budget of two waves per SIMD).
+    constexpr int KS = D / 16;     // links of the scores chain
+    constexpr int PER = 16 / KS;   // scores of block j per link
+    constexpr int NDB = D / 32;    // output blocks
+    constexpr int AHEAD = 2;       // K fragment reads in flight
+    bf16x8_t kf[KS];
+    if (HAS_NEXT) {
+#pragma unroll
+        for (int ks = 0; ks < AHEAD && ks < KS; ++ks) kf[ks] = lds16(kn + ln.kq[ks]);
+    }
+    bf16x8_t va[2][NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+        const bf16x4_t a0 = lds_read_tr(vj + ln.vq[db]);
+        const bf16x4_t a1 = lds_read_tr(vj + ln.vq[db] + 8 * D);
+        va[0][db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    const float neg_mc = st.neg_mc;
+    f32x16_t sn = {};
+    bf16x8_t pf[2];
+    float sum = 0.f;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        if (HAS_NEXT && ks + AHEAD < KS) kf[ks + AHEAD] = lds16(kn + ln.kq[ks + AHEAD]);
+        if (ks == KS / 2) {
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) {
+                const bf16x4_t a0 = lds_read_tr(vj + ln.vq[db] + 16 * D);
+                const bf16x4_t a1 = lds_read_tr(vj + ln.vq[db] + 24 * D);
+                va[1][db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
             }
         }
-        bf16x8_t pf[2];
-        softmax_update<D>(s, c, m, lsum, o, pf);
-        pv_block<D>(stage + G::kTileElems + kb * 32 * D, ln.vq, pf, o);
+        if (HAS_NEXT) sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sn, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int v = ks * PER + u;
+            const float p = fast_exp2(__builtin_fmaf(s[v], c, neg_mc));
+            sum += p;
+            pf[v >> 3][v & 7] = (__bf16)p;
+        }
+        // first half of the weights complete: its PV MFMAs interleave with the remaining links
+        if (ks >= KS / 2 && (ks - KS / 2) < NDB) {
+            const int db = ks - KS / 2;
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[0][db], pf[0], o[db], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+        if (KS / 2 + db >= KS) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[0][db], pf[0], o[db], 0, 0, 0);
+    }
+    st.lsum += sum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[1][db], pf[1], o[db], 0, 0, 0);
+    if (HAS_NEXT) {
+        if (MASK_NEXT) mask_tail(sn, key_next, S, h);
+        block_max_update<D>(sn, c, thr, st, o);
+        s = sn;
     }
 }
 
 struct CacheArgs {
     const uint16_t* kc_base;
     const uint16_t* vc_base;
+    __amdgpu_buffer_rsrc_t krs, vrs;  // the same slices as buffer descriptors
     int kv_stride;
     int S, wave, h;
-    float c;
+    float c, thr;
 };
 
-// Tile t from `cur`; with MORE, tile t+1 (ragged iff NEXT_RAGGED) is loaded into `nxt`
-// meanwhile.  Ends with every load retired and a barrier.
-template <int D, bool RAGGED, bool MORE, bool NEXT_RAGGED>
-__device__ __forceinline__ void cache_step(int t, const CacheArgs& a, const AttnLane<D>& ln, const uint16_t* cur,
-                                           uint16_t* nxt, const bf16x8_t (&qf)[D / 16], float& m, float& lsum,
+// Both bodies of a stage whose blocks 2t, 2t+1, 2t+2 are full cache blocks, with the loads of
+// stage t+1 (full: 64 t + 160 <= S) in flight meanwhile.  Ends with the loads retired and a
+// barrier.
+template <int D>
+__device__ __forceinline__ void full_stage(int t, const CacheArgs& a, const AttnLane<D>& ln, const uint16_t* cur,
+                                           uint16_t* nxt, const bf16x8_t (&qf)[D / 16], f32x16_t& s, SoftState& st,
                                            f32x16_t (&o)[D / 32]) {
-    if (MORE) cache_dma<D, NEXT_RAGGED>(a.kc_base, a.vc_base, a.kv_stride, t + 1, a.S, a.wave, ln, nxt);
-    cache_tile<D, RAGGED>(cur, ln, qf, a.c, t * kAttnTile, a.S, a.h, m, lsum, o);
-    if (MORE) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    using G = AttnGeom<D>;
+    stage_dma<D, false>(a.krs, a.vrs, a.kv_stride, t + 1, a.S, a.wave, ln, nxt);
+    cache_body<D, true, false>(cur, cur + G::kTileElems, ln, qf, a.c, a.thr, 0, a.S, a.h, s, st, o);
+    cache_body<D, true, false>(cur + 32 * D, cur + G::kTileElems + 32 * D, ln, qf, a.c, a.thr, 0, a.S, a.h, s, st,
+                               o);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
 }
 
@@ -290,49 +426,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     const int b = bg / P.Hkv;
     const int N = P.N, L = P.L, S = P.S;
     const float c = P.scale_log2;
+    const float thr = kLazyLog2 / c;  // lazy-rescale margin in raw score units
 
-    // Ancestor masks (bit j of anc[n] set when draft j is n itself or on n's root path).
-    if (tid < N) {
-        uint64_t msk = 1ull << tid;
-        int j = P.parent[(int64_t)b * N + tid];
-        int prev = tid;
-        for (int hops = 0; j != -1 && hops < N; ++hops) {
-            if (j < -1 || j >= prev) {  // not topological: report, stop the walk here
-                flag_device_status(1);
-                break;
-            }
-            msk |= 1ull << j;
-            prev = j;
-            j = P.parent[(int64_t)b * N + j];
-        }
-        anc[tid] = msk;
-    }
+    // The parent array (ancestor walk below) is loaded first: the walk then waits for this
+    // load only, not for the Q, K and stage loads issued after it.
+    const int pj = (wave == 0 && lane < N) ? P.parent[(int64_t)b * N + lane] : -1;
 
     // This lane's query row (lanes l and l^32 share a row).
     const int row = (wg_in_group * kAttnWaves + wave) * 32 + (lane & 31);
     const bool row_valid = row < P.rows_per_group;
     const int NL = N * L;
-    int nd = 0;
-    int64_t row_off = 0;
-    if (row_valid) {
+    // query row -> (head in group, draft, position) and the element offset of its q / out row
+    auto row_offset = [&](int& nd_out) -> int64_t {
         const int hg = row / NL;
         const int rem = row - hg * NL;
-        nd = rem / L;
-        const int p = rem - nd * L;
-        row_off = ((((int64_t)b * N + nd) * L + p) * P.Hq + (g * P.group + hg)) * D;
-    }
+        nd_out = rem / L;
+        const int p = rem - nd_out * L;
+        return ((((int64_t)b * N + nd_out) * L + p) * P.Hq + (g * P.group + hg)) * D;
+    };
+    int nd_q = 0;
+    const int64_t row_off_q = row_valid ? row_offset(nd_q) : 0;
     bf16x8_t qf[D / 16];
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
         if (row_valid) {
-            qf[ks] = __builtin_bit_cast(bf16x8_t, ldg16(P.q + row_off + ks * 16 + h * 8));
+            qf[ks] = __builtin_bit_cast(bf16x8_t, ldg16(P.q + row_off_q + ks * 16 + h * 8));
         } else {
             qf[ks] = bf16x8_t{};
         }
     }
-    // Retire the Q loads here, so that no use of Q inside the tile loop has to wait for the
-    // next tile's loads as well.
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    // The Q loads are retired by the prologue's wait below (together with block 0 and stage 0),
+    // so no use of Q inside the tile loop waits on a later stage's loads.
 
     const int kv_stride = P.Hkv * D;  // elements between consecutive keys
     AttnLane<D> ln;
@@ -355,65 +479,110 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     f32x16_t o[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) o[db] = f32x16_t{};
-    float m = kNegInf, lsum = 0.f;
+    SoftState st = {kNegInf, 0.f, kNegInf, 0.f};
 
     // ---------------- phase 1: cache keys ----------------
     CacheArgs ca;
     ca.kc_base = P.kc + ((int64_t)b * S * P.Hkv + g) * D;
     ca.vc_base = P.vc + ((int64_t)b * S * P.Hkv + g) * D;
     ca.kv_stride = kv_stride;
+    {
+        // descriptors over this (b, g) slice to the end of the tensor (the host guarantees one
+        // sequence's cache spans less than 2^31 bytes, so row offsets fit the 32-bit soffset)
+        const int64_t total = (int64_t)P.B * S * P.Hkv * D * 2;
+        const int64_t start = ((int64_t)b * S * P.Hkv + g) * D * 2;
+        const int64_t rem = total - start;
+        const int nrec = rem > 0x7FFFFFFF ? 0x7FFFFFFF : (int)rem;
+        ca.krs = __builtin_amdgcn_make_buffer_rsrc((void*)ca.kc_base, (short)0, nrec, kBufferFlags);
+        ca.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)ca.vc_base, (short)0, nrec, kBufferFlags);
+    }
     ca.S = S;
     ca.wave = wave;
     ca.h = h;
     ca.c = c;
+    ca.thr = thr;
 
-    const int ntiles = (S + kAttnTile - 1) / kAttnTile;
-    const bool ragged_last = ntiles * kAttnTile != S;
-    if (ntiles > 0) {
-        if (ntiles == 1 && ragged_last) {
-            cache_dma<D, true>(ca.kc_base, ca.vc_base, kv_stride, 0, S, wave, ln, buf0);
+    const int nb = (S + 31) / 32;    // 32-key blocks
+    const int nfull = S / 32;        // full blocks; block nfull is partial when nb > nfull
+    const int nst = (nb + 1) / 2;    // stages
+    f32x16_t s = {};
+    bf16x8_t kf0[D / 16];
+    if (nb > 0) {
+        load_k_global<D>(ca.kc_base, kv_stride, S, lane, kf0);
+        if (96 <= S) {
+            stage_dma<D, false>(ca.krs, ca.vrs, kv_stride, 0, S, wave, ln, buf0);
         } else {
-            cache_dma<D, false>(ca.kc_base, ca.vc_base, kv_stride, 0, S, wave, ln, buf0);
+            stage_dma<D, true>(ca.krs, ca.vrs, kv_stride, 0, S, wave, ln, buf0);
         }
+    }
+    // Ancestor masks (bit j of anc[n] set when draft j is n itself or on n's root path).  Wave 0
+    // holds the sequence's parent array (N <= 64 = one value per lane) and every lane walks
+    // its own draft's chain through lane shuffles, so the walk costs no dependent global loads.
+    if (wave == 0) {
+        uint64_t msk = 1ull << lane;
+        int j = pj, prev = lane;
+        bool live = lane < N;
+        while (true) {  // every step moves prev strictly down, so at most N steps
+            const bool step = live && j != -1;
+            const bool bad = step && (j < -1 || j >= prev);  // not topological: report, stop here
+            if (bad) flag_device_status(1);
+            const bool go = step && !bad;
+            if (ballot64(go) == 0ull) break;
+            if (go) {
+                msk |= 1ull << j;
+                prev = j;
+            }
+            const int nj = __shfl(pj, go ? j : 0);
+            j = go ? nj : -1;
+            live = go;
+        }
+        if (lane < N) anc[lane] = msk;
+    }
+    if (nb > 0) {
+        s = qk_frags<D>(kf0, qf);
+        if (nfull == 0) mask_tail(s, 0, S, h);
+        block_max_update<D>(s, c, thr, st, o);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     }
     __syncthreads();
-    if (ntiles > 0) {
-        // Tiles 0 .. ntiles-2 are full and each loads its successor.  The main loop runs them
-        // in pairs (buffers 0 and 1) while both successors are full, so its body has no
-        // conditional code; the 0-2 remaining full tiles follow, and only the step that loads
-        // the last tile needs to know whether that tile is ragged.
-        int t = 0;
-        for (; t + 2 < ntiles - 1; t += 2) {
-            cache_step<D, false, true, false>(t, ca, ln, buf0, buf1, qf, m, lsum, o);
-            cache_step<D, false, true, false>(t + 1, ca, ln, buf1, buf0, qf, m, lsum, o);
-        }
-        const int rest = ntiles - 1 - t;  // 0, 1 or 2 full tiles before the last one
-        if (rest == 2) {
-            cache_step<D, false, true, false>(t, ca, ln, buf0, buf1, qf, m, lsum, o);
-            if (ragged_last) {
-                cache_step<D, false, true, true>(t + 1, ca, ln, buf1, buf0, qf, m, lsum, o);
+    int t = 0;
+    // Stage pairs whose successors are full: buffers known at compile time, no conditional code.
+    for (; 64 * t + 224 <= S; t += 2) {
+        full_stage<D>(t, ca, ln, buf0, buf1, qf, s, st, o);
+        full_stage<D>(t + 1, ca, ln, buf1, buf0, qf, s, st, o);
+    }
+    // Remaining stages (at most three of them): per-block checks for the last block, the
+    // partial block and the clamped loads.
+    for (; t < nst; ++t) {
+        uint16_t* cur = (t & 1) ? buf1 : buf0;
+        uint16_t* nxt = (t & 1) ? buf0 : buf1;
+        if (t + 1 < nst) {
+            if (64 * t + 160 <= S) {
+                stage_dma<D, false>(ca.krs, ca.vrs, kv_stride, t + 1, S, wave, ln, nxt);
             } else {
-                cache_step<D, false, true, false>(t + 1, ca, ln, buf1, buf0, qf, m, lsum, o);
+                stage_dma<D, true>(ca.krs, ca.vrs, kv_stride, t + 1, S, wave, ln, nxt);
             }
-            t += 2;
-        } else if (rest == 1) {
-            if (ragged_last) {
-                cache_step<D, false, true, true>(t, ca, ln, buf0, buf1, qf, m, lsum, o);
+        }
+        for (int half = 0; half < 2; ++half) {
+            const int j = 2 * t + half;
+            if (j >= nb) break;
+            const uint16_t* kn = cur + half * 32 * D;
+            const uint16_t* vj = cur + G::kTileElems + half * 32 * D;
+            if (j + 1 >= nb) {
+                cache_body<D, false, false>(kn, vj, ln, qf, c, thr, 0, S, h, s, st, o);
+            } else if (j + 1 == nfull) {
+                cache_body<D, true, true>(kn, vj, ln, qf, c, thr, 32 * (j + 1), S, h, s, st, o);
             } else {
-                cache_step<D, false, true, false>(t, ca, ln, buf0, buf1, qf, m, lsum, o);
+                cache_body<D, true, false>(kn, vj, ln, qf, c, thr, 0, S, h, s, st, o);
             }
-            t += 1;
         }
-        const uint16_t* last = (t & 1) ? buf1 : buf0;
-        if (ragged_last) {
-            cache_step<D, true, false, false>(t, ca, ln, last, nullptr, qf, m, lsum, o);
-        } else {
-            cache_step<D, false, false, false>(t, ca, ln, last, nullptr, qf, m, lsum, o);
-        }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
     }
 
     // ---------------- phase 2: draft blocks on the root path ----------------
+    int nd = 0;
+    if (row_valid) (void)row_offset(nd);
     const uint64_t my_anc = row_valid ? anc[nd] : 0ull;
     const uint64_t U = wave_or64(my_anc);
     uint16_t* kw = (wave < 2 ? buf0 : buf1) + (wave & 1) * G::kWaveRegionElems;
@@ -422,13 +591,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     const uint16_t* vd_base = P.vd + (int64_t)g * D;
     const int wri = lane / G::kChunks;
     const int wpc = lane % G::kChunks;
-    const int dtiles = (NL + 31) / 32;
-    for (int tt = 0; tt < dtiles; ++tt) {
+    // Visit the 32-key tiles that hold a block of U (any row's root path), in ascending order:
+    // the blocks of U are taken lowest first and each covers tiles (j L) / 32 .. (j L + L - 1) / 32,
+    // skipping tiles an earlier block already covered.
+    uint64_t todo = U;  // wave-uniform
+    int next_tile = 0;
+    while (todo != 0ull) {
+      const int jb = __builtin_ctzll(todo);
+      todo &= todo - 1ull;
+      const int t_hi = (jb * L + L - 1) >> 5;
+      for (int tt = max((jb * L) >> 5, next_tile); tt <= t_hi; ++tt) {
         const int k0 = tt * 32;
         const int jlo = k0 / L;
         const int jhi = min(N - 1, (k0 + 31) / L);
         const uint64_t T = (jhi - jlo == 63) ? ~0ull : (((1ull << (jhi - jlo + 1)) - 1) << jlo);
-        if ((U & T) == 0) continue;  // wave-uniform
         const bool lane_full = !row_valid || ((my_anc & T) == T);
         const bool all_full = ballot64_all(lane_full);
         const bool full = (k0 + 32 <= NL) & all_full;
@@ -469,14 +645,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
             }
         }
         bf16x8_t pf[2];
-        softmax_update<D>(s, c, m, lsum, o, pf);
+        softmax_update<D>(s, c, thr, st, o, pf);
         pv_block<D>(vw, ln.vq, pf, o);
+      }
+      next_tile = max(next_tile, t_hi + 1);
     }
 
     // ---------------- epilogue ----------------
-    const float l = pair_sum(lsum);
+    const float l = pair_sum(st.lsum);
     const float inv = l > 0.f ? 1.0f / l : 0.f;
     if (row_valid) {
+        int nd_o = 0;
+        const int64_t row_off = row_offset(nd_o);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
 #pragma unroll

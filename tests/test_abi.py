@@ -62,6 +62,8 @@ def test_attention_argument_errors():
     assert call(_lib.AttnShape(1, 65, 8, 4, 4, 64, 192, 0.0)) == 2   # N > 64
     assert call(_lib.AttnShape(1, 4, 0, 4, 4, 64, 192, 0.0)) == 2    # L = 0
     assert call(_lib.AttnShape(1, 4, 8, 4, 4, 96, 192, 0.0)) == 4    # head dim
+    # one sequence's cache slice (S * Hkv * D * 2 bytes) is addressed with 32-bit offsets
+    assert call(_lib.AttnShape(1, 4, 8, 8, 8, 128, 1 << 20, 0.0)) == 4
     assert call(_lib.AttnShape(1, 4, 8, 4, 4, 64, 192, float("nan"))) == 7
     mis = [ctypes.c_void_p(0x1002)] + [FAKE] * 6
     assert call(good, mis) == 2                                       # misaligned q
