@@ -4,7 +4,10 @@
 //
 // HBM-bound streaming design for gfx950:
 //   * one 256-thread workgroup streams one row (or one slice of a row when there are too
-//     few rows to fill 256 CUs) with 16-byte non-temporal loads, four in flight per lane;
+//     few rows to fill 256 CUs) with 16-byte non-temporal loads: full sweeps of the
+//     workgroup load unconditionally, two vectors per lane per sweep, and the next sweep's
+//     loads are issued before the current sweep is absorbed (a guard per load would put each
+//     load in its own branch and serialise them); only the last, partial sweep checks bounds;
 //   * each lane keeps a running (max, rescaled sum) and a sorted top-K list; a vector of 8
 //     bf16 costs one max-tree, one rescale test, 8 fma+exp2+add and one compare against
 //     the lane's current K-th value (insertions are rare after the first few vectors);
@@ -18,7 +21,7 @@
 namespace trajspec {
 
 constexpr int kTopkThreads = 256;
-constexpr int kTopkUnroll = 4;
+constexpr int kTopkUnroll = 2;
 constexpr int kTopkRecord = 2 + 2 * 8;  // floats per partial record: m, s, 8 64-bit keys
 
 // A candidate is packed into one 64-bit key whose unsigned order is the selection order:
@@ -140,17 +143,23 @@ __device__ __forceinline__ void absorb(const float (&x)[NV], int id0, float& m, 
 // Lower bound on the k-th largest value of a row from the lanes' running maxima: the k-th
 // largest lane maximum (all copies of each round's maximum are dropped, which can only
 // lower the bound).  Returned in order_bits form; 0 when fewer than k lanes hold a value.
+// (K >= k bounds the rounds at compile time: no inner loop, which keeps the compiler's
+// load-wait placement exact in the streaming loop around it.)
+template <int K>
 __device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
     uint32_t cur = lane_max == kNegInf ? 0u : order_bits(lane_max);
     uint32_t best = 0;
-    for (int r = 0; r < k; ++r) {
-        best = cur;
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const uint32_t o = __shfl_xor(best, off);
-            best = o > best ? o : best;
+    for (int r = 0; r < K; ++r) {
+        if (r < k) {
+            best = cur;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                const uint32_t o = __shfl_xor(best, off);
+                best = o > best ? o : best;
+            }
+            if (cur == best) cur = 0u;
         }
-        if (cur == best) cur = 0u;
     }
     return best;
 }
@@ -201,8 +210,43 @@ __global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
     if (VECTOR) {
         const int nvec = (end - begin) / NV;
         const u32x4_t* vp = reinterpret_cast<const u32x4_t*>(base + begin);
+        constexpr int SW = kTopkThreads * kTopkUnroll;  // vectors per sweep of the workgroup
+        const int nfull = nvec / SW;
         int it = 0;
-        for (int vb = 0; vb < nvec; vb += kTopkThreads * kTopkUnroll, ++it) {
+        // Full sweeps: unconditional loads, the next sweep's loads in flight while the current
+        // one is absorbed (two register sets, so the loop is unrolled by two).
+        auto load_sweep = [&](int sweep, u32x4_t (&buf)[kTopkUnroll]) {
+#pragma unroll
+            for (int u = 0; u < kTopkUnroll; ++u) buf[u] = __builtin_nontemporal_load(vp + sweep * SW + u * kTopkThreads + tid);
+        };
+        auto absorb_sweep = [&](int sweep, const u32x4_t (&buf)[kTopkUnroll]) {
+#pragma unroll
+            for (int u = 0; u < kTopkUnroll; ++u) {
+                float x[NV];
+                unpack(buf[u], x);
+                absorb<K, NV>(x, begin + (sweep * SW + u * kTopkThreads + tid) * NV, m, s, tl, floor_bits);
+            }
+            // refresh the wave floor after sweeps 0, 1, 3, 7, 15, ...
+            if ((sweep & (sweep + 1)) == 0) floor_bits = wave_kth_floor<K>(m, k);
+        };
+        if (nfull > 0) {
+            u32x4_t bufa[kTopkUnroll], bufb[kTopkUnroll];
+            load_sweep(0, bufa);
+            for (; it + 2 <= nfull; it += 2) {
+                load_sweep(it + 1, bufb);
+                __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the absorb
+                absorb_sweep(it, bufa);
+                if (it + 2 < nfull) load_sweep(it + 2, bufa);
+                __builtin_amdgcn_sched_barrier(0);
+                absorb_sweep(it + 1, bufb);
+            }
+            if (it < nfull) {  // odd count: the last full sweep is already loaded in bufa
+                absorb_sweep(it, bufa);
+                ++it;
+            }
+        }
+        // Last, partial sweep: per-vector bounds.
+        for (int vb = nfull * SW; vb < nvec; vb += SW, ++it) {
             u32x4_t buf[kTopkUnroll];
 #pragma unroll
             for (int u = 0; u < kTopkUnroll; ++u) {
@@ -218,8 +262,7 @@ __global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
                     absorb<K, NV>(x, begin + vi * NV, m, s, tl, floor_bits);
                 }
             }
-            // refresh the wave floor after iterations 0, 1, 3, 7, 15, ...
-            if ((it & (it + 1)) == 0) floor_bits = wave_kth_floor(m, k);
+            if ((it & (it + 1)) == 0) floor_bits = wave_kth_floor<K>(m, k);
         }
         scalar_from = begin + nvec * NV;
     }
