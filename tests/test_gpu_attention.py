@@ -193,3 +193,30 @@ def test_cache_lengths_cover_every_tail_path(S):
         inputs, _, out = _run(wl, 1000 + S, variant, parent=parent)
         ok, worst, frac = _check(out, inputs, parent, variant)
         assert ok, f"S={S} {variant}: worst excess {worst:.3g}, {frac:.2%} bad"
+
+
+@pytest.mark.parametrize("where", ["block0", "main_loop", "tail_stage", "partial_block", "ancestor_draft", "own_draft"])
+def test_reference_moves_late(where):
+    """Keys whose scores jump far above every earlier block (about 25 powers of two on the
+    sharp inputs) force the lazy reference to move and O and the running sum to be rescaled at
+    that point: in the first block, inside the paired stage loop, in the tail stages, in the
+    partial last block, or in the draft phase.  The result must still match the oracle."""
+    wl = Workload(97, "jump", B=1, N=4, L=32, Hq=2, Hkv=1, D=128, S_prefix=700, S_suffix=0, V=64,
+                  logits_dtype="f32", margin_max=3.0, parents=(-1, 0, 1, 1), level_sizes=None)
+    parent = np.array([[-1, 0, 1, 1]], dtype=np.int32)
+    q, kc, vc, kd, vd = attention_inputs(wl, 4242, "sharp")
+    # 700 keys = 22 blocks of 32: blocks 0-15 run in the paired stage loop, 16-21 in the tail
+    # stages, block 21 is partial (keys 672-699)
+    sel = {"block0": (kc, slice(0, 32)), "main_loop": (kc, slice(200, 210)), "tail_stage": (kc, slice(580, 600)),
+           "partial_block": (kc, slice(680, 690)), "ancestor_draft": (kd, 1), "own_draft": (kd, 3)}[where]
+    t, idx = sel
+    kc, kd = kc.clone(), kd.clone()
+    if t is kc:
+        kc[0, idx] = (kc[0, idx].float() * 3.0).to(torch.bfloat16)
+    else:
+        kd[0, idx] = (kd[0, idx].float() * 3.0).to(torch.bfloat16)
+    inputs = (q, kc, vc, kd, vd)
+    out = tsp.verify_attn(*[x.cuda() for x in inputs], cuda(parent, torch.int32))
+    torch.cuda.synchronize()
+    ok, worst, frac = _check(out, inputs, parent, "sharp")
+    assert ok, f"{where}: worst excess {worst:.3g}, {frac:.2%} outside tolerance"
