@@ -323,6 +323,7 @@ __global__ __launch_bounds__(64) void conf_topk_merge_kernel(const float* __rest
                                                              int splits, int k, float* __restrict__ conf,
                                                              int32_t* __restrict__ idx) {
     const int row = blockIdx.x;
+    if (row >= rows) return;  // the grid is exactly `rows`; kept for any other launch shape
     const int lane = threadIdx.x;
     float m = kNegInf, s = 0.f;
     TopList<K> tl;

@@ -97,7 +97,9 @@ def test_strided_and_unaligned_rows_use_scalar_path():
     _check(f32, 2, label="fp32 unaligned")
 
 
-@pytest.mark.parametrize("V", [1, 7, 255, 1000, 2049])
+# 4096 / 8200 / 12300 give 1, 2 and 3 full workgroup sweeps (bf16; fp32 twice as many) with
+# and without a remainder, so the double-buffered sweep loop and its odd tail are exercised.
+@pytest.mark.parametrize("V", [1, 7, 255, 1000, 2049, 4096, 8200, 12300])
 def test_small_and_ragged_vocab(V):
     rng = np.random.default_rng(V)
     x = torch.from_numpy(rng.standard_normal((40, V)).astype(np.float32))
