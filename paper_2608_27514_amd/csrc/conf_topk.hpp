@@ -354,10 +354,13 @@ struct TopkPlan {
     int chunk;
 };
 
-// Splits short batches so that at least ~2048 workgroups stream the rows.
+// Splits short batches so that at least ~512 workgroups stream the rows.  More, shorter
+// slices cost more than they gain: each slice pays a workgroup reduction and a partial record,
+// and the merge kernel grows with them (measured on 256-1024-row batches: a 2048 target was
+// 15-25% slower than 512).
 inline TopkPlan plan_conf_topk(int64_t rows, int64_t vocab, int vec) {
     TopkPlan p{1, (int)vocab};
-    const int64_t target = 2048;
+    const int64_t target = 512;
     if (rows <= 0 || rows >= target) return p;
     const int64_t align = (int64_t)kTopkThreads * vec;  // one full sweep of the workgroup
     int64_t want = (target + rows - 1) / rows;
