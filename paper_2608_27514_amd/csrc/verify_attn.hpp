@@ -157,13 +157,10 @@ struct SoftState {
 // kLazyLog2 / c in raw score units; with m = -inf the test holds exactly when the block has
 // a visible key.
 
+// Folds a block maximum mx (already combined with lane^32) into `m`, rescaling o and lsum when
+// it moves past the lazy trigger.
 template <int D>
-__device__ __forceinline__ void block_max_update(const f32x16_t& s, float c, float thr, SoftState& st,
-                                                 f32x16_t (&o)[D / 32]) {
-    float mx = __builtin_elementwise_maximum(s[0], s[1]);
-#pragma unroll
-    for (int v = 2; v < 16; v += 2) mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, s[v]), s[v + 1]);
-    mx = pair_max(mx);
+__device__ __forceinline__ void fold_max(float mx, float c, float thr, SoftState& st, f32x16_t (&o)[D / 32]) {
     const bool need = mx > st.mthr;
     if (ballot64(need) != 0ull) {
         const float m_new = need ? mx : st.m;
@@ -175,6 +172,21 @@ __device__ __forceinline__ void block_max_update(const f32x16_t& s, float c, flo
         st.neg_mc = m_new == kNegInf ? 0.f : -m_new * c;
         st.mthr = m_new + thr;
     }
+}
+
+__device__ __forceinline__ float max16(const f32x16_t& s, float mx) {
+#pragma unroll
+    for (int v = 0; v < 16; v += 2) mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, s[v]), s[v + 1]);
+    return mx;
+}
+
+template <int D>
+__device__ __forceinline__ void block_max_update(const f32x16_t& s, float c, float thr, SoftState& st,
+                                                 f32x16_t (&o)[D / 32]) {
+    float mx = __builtin_elementwise_maximum(s[0], s[1]);
+#pragma unroll
+    for (int v = 2; v < 16; v += 2) mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, s[v]), s[v + 1]);
+    fold_max<D>(pair_max(mx), c, thr, st, o);
 }
 
 // block_exp: weights of one block against the current reference (neg_mc = -c*m); pf[half]
@@ -274,135 +286,118 @@ __device__ __forceinline__ void cache_rows_dma(__amdgpu_buffer_rsrc_t rs, int kv
     }
 }
 
-// Stage t of the cache pipeline holds the K rows of keys 64 t + 32 .. 64 t + 95 (blocks 2t+1
-// and 2t+2) and the V rows of keys 64 t .. 64 t + 63 (blocks 2t and 2t+1): block j's body
-// multiplies V of block j and computes the scores of block j+1, so both bodies of a stage
-// read one buffer and a single barrier per stage suffices.  RAGGED when 64 t + 96 > S.
+// Stage t of the cache pipeline holds the V rows of keys 64 t .. 64 t + 63 (blocks 2t, 2t+1) and
+// the K rows of keys 64 t + 64 .. 64 t + 127 (blocks 2t+2, 2t+3): the matrix phase of step t
+// multiplies the V rows of the blocks whose weights were just computed and the K rows of the
+// next two blocks, so one buffer and one barrier per stage suffice.  RAGGED when 64 t + 128 > S.
 template <int D, bool RAGGED>
 __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t vrs, int kv_stride, int t,
                                           int S, int wave, const AttnLane<D>& ln, uint16_t* stage) {
     using G = AttnGeom<D>;
-    cache_rows_dma<D, RAGGED, false>(krs, kv_stride, t * kAttnTile + 32, S, wave, ln, stage);
+    cache_rows_dma<D, RAGGED, false>(krs, kv_stride, t * kAttnTile + kAttnTile, S, wave, ln, stage);
     cache_rows_dma<D, RAGGED, true>(vrs, kv_stride, t * kAttnTile, S, wave, ln, stage + G::kTileElems);
 }
 
-// K fragments of cache keys 0..31 straight from global memory (the first block of the
-// pipeline, needed before any stage is in LDS), and S^T of a block from such fragments; keys
-// >= S read key S-1 and are masked by the caller.
+// Softmax phase of a 64-key step: the scores of two blocks (s[0], s[1]) against the query's
+// reference, after folding their joint maximum into it; pf[b][half] receives the bf16 weights
+// of block b, keys 16 half .. 16 half + 15, in MFMA B-operand order.
 template <int D>
-__device__ __forceinline__ void load_k_global(const uint16_t* kc_base, int kv_stride, int S, int lane,
-                                              bf16x8_t (&kf)[D / 16]) {
-    const int key = min(lane & 31, S - 1);
-    const uint16_t* p = kc_base + (int64_t)key * kv_stride + 8 * (lane >> 5);
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) kf[ks] = __builtin_bit_cast(bf16x8_t, ldg16(p + 16 * ks));
-}
-
-template <int D>
-__device__ __forceinline__ f32x16_t qk_frags(const bf16x8_t (&kf)[D / 16], const bf16x8_t (&qf)[D / 16]) {
-    f32x16_t s = {};
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], s, 0, 0, 0);
-    return s;
-}
-
-// Body of cache block j, software-pipelined: `s` holds the scores of block j (its maximum
-// already folded into m).  The scores of block j+1 (K rows at kn) are issued on the matrix
-// cores, block j's weights are computed on the vector ALUs between the links of that chain,
-// then O += V_j P_j (V rows at vj); finally block j+1's maximum is folded in and `s` becomes
-// block j+1.
-template <int D, bool HAS_NEXT, bool MASK_NEXT>
-__device__ __forceinline__ void cache_body(const uint16_t* kn, const uint16_t* vj, const AttnLane<D>& ln,
-                                           const bf16x8_t (&qf)[D / 16], float c, float thr, int key_next, int S,
-                                           int h, f32x16_t& s, SoftState& st, f32x16_t (&o)[D / 32]) {
-    // A wave issues in order and an MFMA waits for the matrix core, so the body is written in
-    // the order it should issue: the links of the scores chain of block j+1 alternate with the
-    // weights of block j (PER scores per link) and, once the first half of the weights is
-    // ready, with the first half of O += V_j P_j.  Fragment reads run a few links ahead.
-    // sched_barrier(0) keeps the compiler from regrouping (hoisting every read raises register
-    // pressure beyond the budget of two waves per SIMD).
-    constexpr int KS = D / 16;     // links of the scores chain
-    constexpr int PER = 16 / KS;   // scores of block j per link
-    constexpr int NDB = D / 32;    // output blocks
-    constexpr int AHEAD = 2;       // K fragment reads in flight
-    bf16x8_t kf[KS];
-    if (HAS_NEXT) {
-#pragma unroll
-        for (int ks = 0; ks < AHEAD && ks < KS; ++ks) kf[ks] = lds16(kn + ln.kq[ks]);
-    }
-    bf16x8_t va[2][NDB];
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-        const bf16x4_t a0 = lds_read_tr(vj + ln.vq[db]);
-        const bf16x4_t a1 = lds_read_tr(vj + ln.vq[db] + 8 * D);
-        va[0][db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
+__device__ __forceinline__ void softmax_phase(const f32x16_t (&s)[2], float c, float thr, SoftState& st,
+                                              f32x16_t (&o)[D / 32], bf16x8_t (&pf)[2][2]) {
+    const float mx = max16(s[1], max16(s[0], kNegInf));
+    fold_max<D>(pair_max(mx), c, thr, st, o);
     const float neg_mc = st.neg_mc;
-    f32x16_t sn = {};
-    bf16x8_t pf[2];
-    float sum = 0.f;
-    __builtin_amdgcn_sched_barrier(0);
+    float sum0 = 0.f, sum1 = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const float p0 = fast_exp2(__builtin_fmaf(s[0][v], c, neg_mc));
+        const float p1 = fast_exp2(__builtin_fmaf(s[1][v], c, neg_mc));
+        sum0 += p0;
+        sum1 += p1;
+        pf[0][v >> 3][v & 7] = (__bf16)p0;
+        pf[1][v >> 3][v & 7] = (__bf16)p1;
+    }
+    st.lsum += sum0 + sum1;
+}
+
+// Scores of two consecutive 32-key blocks whose K rows start at kbase (rows 0..31, 32..63 of a K
+// region): two independent MFMA chains, links alternating, fragment reads two links ahead.
+template <int D>
+__device__ __forceinline__ void qk_pair(const uint16_t* kbase, const AttnLane<D>& ln, const bf16x8_t (&qf)[D / 16],
+                                        f32x16_t (&sn)[2]) {
+    constexpr int KS = D / 16;
+    bf16x8_t ka[KS], kb[KS];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        ka[ks] = lds16(kbase + ln.kq[ks]);
+        kb[ks] = lds16(kbase + 32 * D + ln.kq[ks]);
+    }
+    f32x16_t a = {}, b = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-        if (HAS_NEXT && ks + AHEAD < KS) kf[ks + AHEAD] = lds16(kn + ln.kq[ks + AHEAD]);
-        if (ks == KS / 2) {
-#pragma unroll
-            for (int db = 0; db < NDB; ++db) {
-                const bf16x4_t a0 = lds_read_tr(vj + ln.vq[db] + 16 * D);
-                const bf16x4_t a1 = lds_read_tr(vj + ln.vq[db] + 24 * D);
-                va[1][db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-            }
+        if (ks + 2 < KS) {
+            ka[ks + 2] = lds16(kbase + ln.kq[ks + 2]);
+            kb[ks + 2] = lds16(kbase + 32 * D + ln.kq[ks + 2]);
         }
-        if (HAS_NEXT) sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sn, 0, 0, 0);
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const int v = ks * PER + u;
-            const float p = fast_exp2(__builtin_fmaf(s[v], c, neg_mc));
-            sum += p;
-            pf[v >> 3][v & 7] = (__bf16)p;
-        }
-        // first half of the weights complete: its PV MFMAs interleave with the remaining links
-        if (ks >= KS / 2 && (ks - KS / 2) < NDB) {
-            const int db = ks - KS / 2;
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[0][db], pf[0], o[db], 0, 0, 0);
-        }
+        a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], a, 0, 0, 0);
+        b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[ks], qf[ks], b, 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
     }
+    sn[0] = a;
+    sn[1] = b;
+}
+
+// O^T += V^T P^T for two consecutive 32-key blocks whose V rows start at vbase; each (block,
+// half) group's transposing reads are issued one group ahead of its MFMAs.
+template <int D>
+__device__ __forceinline__ void pv_pair(const uint16_t* vbase, const AttnLane<D>& ln, const bf16x8_t (&pf)[2][2],
+                                        f32x16_t (&o)[D / 32]) {
+    constexpr int NDB = D / 32;
+    bf16x8_t va[2][NDB];
+    auto read_group = [&](int grp, bf16x8_t (&dst)[NDB]) {
+        const uint16_t* base = vbase + (grp >> 1) * 32 * D + (grp & 1) * 16 * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-        if (KS / 2 + db >= KS) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[0][db], pf[0], o[db], 0, 0, 0);
-    }
-    st.lsum += sum;
+        for (int db = 0; db < NDB; ++db) {
+            const bf16x4_t a0 = lds_read_tr(base + ln.vq[db]);
+            const bf16x4_t a1 = lds_read_tr(base + ln.vq[db] + 8 * D);
+            dst[db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+    };
+    read_group(0, va[0]);
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[1][db], pf[1], o[db], 0, 0, 0);
-    if (HAS_NEXT) {
-        if (MASK_NEXT) mask_tail(sn, key_next, S, h);
-        block_max_update<D>(sn, c, thr, st, o);
-        s = sn;
+    for (int grp = 0; grp < 4; ++grp) {
+        if (grp + 1 < 4) read_group(grp + 1, va[(grp + 1) & 1]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[grp & 1][db], pf[grp >> 1][grp & 1], o[db], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
 struct CacheArgs {
-    const uint16_t* kc_base;
-    const uint16_t* vc_base;
-    __amdgpu_buffer_rsrc_t krs, vrs;  // the same slices as buffer descriptors
+    __amdgpu_buffer_rsrc_t krs, vrs;  // this (b, g) cache slice as buffer descriptors
     int kv_stride;
     int S, wave, h;
     float c, thr;
 };
 
-// Both bodies of a stage whose blocks 2t, 2t+1, 2t+2 are full cache blocks, with the loads of
-// stage t+1 (full: 64 t + 160 <= S) in flight meanwhile.  Ends with the loads retired and a
-// barrier.
+// One 64-key step t of the cache phase whose next stage is full (64 t + 192 <= S): the loads of
+// stage t+1 go out, the softmax phase turns the scores of blocks 2t, 2t+1 into weights, the
+// matrix phase computes the scores of blocks 2t+2, 2t+3 and adds the weighted V rows of blocks
+// 2t, 2t+1.  Ends with the loads retired and a barrier.  Two waves of different workgroups
+// share each SIMD: one's softmax phase runs on the vector ALU while the other's matrix phase
+// runs on the matrix core.
 template <int D>
-__device__ __forceinline__ void full_stage(int t, const CacheArgs& a, const AttnLane<D>& ln, const uint16_t* cur,
-                                           uint16_t* nxt, const bf16x8_t (&qf)[D / 16], f32x16_t& s, SoftState& st,
-                                           f32x16_t (&o)[D / 32]) {
+__device__ __forceinline__ void full_step(int t, const CacheArgs& a, const AttnLane<D>& ln, const uint16_t* cur,
+                                          uint16_t* nxt, const bf16x8_t (&qf)[D / 16], f32x16_t (&s)[2], SoftState& st,
+                                          f32x16_t (&o)[D / 32]) {
     using G = AttnGeom<D>;
     stage_dma<D, false>(a.krs, a.vrs, a.kv_stride, t + 1, a.S, a.wave, ln, nxt);
-    cache_body<D, true, false>(cur, cur + G::kTileElems, ln, qf, a.c, a.thr, 0, a.S, a.h, s, st, o);
-    cache_body<D, true, false>(cur + 32 * D, cur + G::kTileElems + 32 * D, ln, qf, a.c, a.thr, 0, a.S, a.h, s, st,
-                               o);
+    bf16x8_t pf[2][2];
+    softmax_phase<D>(s, a.c, a.thr, st, o, pf);
+    __builtin_amdgcn_sched_barrier(0);
+    qk_pair<D>(cur, ln, qf, s);
+    pv_pair<D>(cur + G::kTileElems, ln, pf, o);
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
 }
@@ -483,19 +478,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
 
     // ---------------- phase 1: cache keys ----------------
     CacheArgs ca;
-    ca.kc_base = P.kc + ((int64_t)b * S * P.Hkv + g) * D;
-    ca.vc_base = P.vc + ((int64_t)b * S * P.Hkv + g) * D;
-    ca.kv_stride = kv_stride;
     {
         // descriptors over this (b, g) slice to the end of the tensor (the host guarantees one
         // sequence's cache spans less than 2^31 bytes, so row offsets fit the 32-bit soffset)
+        const uint16_t* kc_base = P.kc + ((int64_t)b * S * P.Hkv + g) * D;
+        const uint16_t* vc_base = P.vc + ((int64_t)b * S * P.Hkv + g) * D;
         const int64_t total = (int64_t)P.B * S * P.Hkv * D * 2;
         const int64_t start = ((int64_t)b * S * P.Hkv + g) * D * 2;
         const int64_t rem = total - start;
         const int nrec = rem > 0x7FFFFFFF ? 0x7FFFFFFF : (int)rem;
-        ca.krs = __builtin_amdgcn_make_buffer_rsrc((void*)ca.kc_base, (short)0, nrec, kBufferFlags);
-        ca.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)ca.vc_base, (short)0, nrec, kBufferFlags);
+        ca.krs = __builtin_amdgcn_make_buffer_rsrc((void*)kc_base, (short)0, nrec, kBufferFlags);
+        ca.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vc_base, (short)0, nrec, kBufferFlags);
     }
+    ca.kv_stride = kv_stride;
     ca.S = S;
     ca.wave = wave;
     ca.h = h;
@@ -503,13 +498,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     ca.thr = thr;
 
     const int nb = (S + 31) / 32;    // 32-key blocks
-    const int nfull = S / 32;        // full blocks; block nfull is partial when nb > nfull
-    const int nst = (nb + 1) / 2;    // stages
-    f32x16_t s = {};
-    bf16x8_t kf0[D / 16];
+    const int nst = (nb + 1) / 2;    // 64-key steps, one stage each
+    f32x16_t s[2] = {{}, {}};        // scores of the step's two blocks
     if (nb > 0) {
-        load_k_global<D>(ca.kc_base, kv_stride, S, lane, kf0);
-        if (96 <= S) {
+        // the K rows of keys 0..63 go to buf1's K region (free until stage 1), stage 0 to buf0
+        if (64 <= S) {
+            cache_rows_dma<D, false, false>(ca.krs, kv_stride, 0, S, wave, ln, buf1);
+        } else {
+            cache_rows_dma<D, true, false>(ca.krs, kv_stride, 0, S, wave, ln, buf1);
+        }
+        if (128 <= S) {
             stage_dma<D, false>(ca.krs, ca.vrs, kv_stride, 0, S, wave, ln, buf0);
         } else {
             stage_dma<D, true>(ca.krs, ca.vrs, kv_stride, 0, S, wave, ln, buf0);
@@ -539,43 +537,45 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
         if (lane < N) anc[lane] = msk;
     }
     if (nb > 0) {
-        s = qk_frags<D>(kf0, qf);
-        if (nfull == 0) mask_tail(s, 0, S, h);
-        block_max_update<D>(s, c, thr, st, o);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        qk_pair<D>(buf1, ln, qf, s);
+        if (S < 64) {
+            mask_tail(s[0], 0, S, h);
+            mask_tail(s[1], 32, S, h);
+        }
     }
-    __syncthreads();
+    __syncthreads();  // buf1 free for stage 1; the ancestor masks visible
     int t = 0;
-    // Stage pairs whose successors are full: buffers known at compile time, no conditional code.
-    for (; 64 * t + 224 <= S; t += 2) {
-        full_stage<D>(t, ca, ln, buf0, buf1, qf, s, st, o);
-        full_stage<D>(t + 1, ca, ln, buf1, buf0, qf, s, st, o);
+    // Step pairs whose next stages are full: buffers known at compile time, no conditional code.
+    for (; 64 * t + 256 <= S; t += 2) {
+        full_step<D>(t, ca, ln, buf0, buf1, qf, s, st, o);
+        full_step<D>(t + 1, ca, ln, buf1, buf0, qf, s, st, o);
     }
-    // Remaining stages (at most three of them): per-block checks for the last block, the
-    // partial block and the clamped loads.
+    // Remaining steps (at most three): clamped loads, masked scores of blocks reaching past S,
+    // no scores after the last block.  Blocks past S get weight 0 (their scores are masked and
+    // their clamped K / V rows are finite).
     for (; t < nst; ++t) {
         uint16_t* cur = (t & 1) ? buf1 : buf0;
         uint16_t* nxt = (t & 1) ? buf0 : buf1;
         if (t + 1 < nst) {
-            if (64 * t + 160 <= S) {
+            if (64 * t + 192 <= S) {
                 stage_dma<D, false>(ca.krs, ca.vrs, kv_stride, t + 1, S, wave, ln, nxt);
             } else {
                 stage_dma<D, true>(ca.krs, ca.vrs, kv_stride, t + 1, S, wave, ln, nxt);
             }
         }
-        for (int half = 0; half < 2; ++half) {
-            const int j = 2 * t + half;
-            if (j >= nb) break;
-            const uint16_t* kn = cur + half * 32 * D;
-            const uint16_t* vj = cur + G::kTileElems + half * 32 * D;
-            if (j + 1 >= nb) {
-                cache_body<D, false, false>(kn, vj, ln, qf, c, thr, 0, S, h, s, st, o);
-            } else if (j + 1 == nfull) {
-                cache_body<D, true, true>(kn, vj, ln, qf, c, thr, 32 * (j + 1), S, h, s, st, o);
-            } else {
-                cache_body<D, true, false>(kn, vj, ln, qf, c, thr, 0, S, h, s, st, o);
+        bf16x8_t pf[2][2];
+        softmax_phase<D>(s, c, thr, st, o, pf);
+        __builtin_amdgcn_sched_barrier(0);
+        if (2 * t + 2 < nb) {
+            qk_pair<D>(cur, ln, qf, s);
+            if (64 * t + 128 > S) {
+                mask_tail(s[0], 64 * t + 64, S, h);
+                mask_tail(s[1], 64 * t + 96, S, h);
             }
         }
+        pv_pair<D>(cur + G::kTileElems, ln, pf, o);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
     }
