@@ -12,6 +12,9 @@ Decoding for Diffusion LLMs):
 * :mod:`oracle.accept`     -- threshold decoding with top-1 fallback (Sec. 2.1),
   child consistency, greedy / longest-path traversal (Sec. 3.3 "Verification
   procedure"), the next root's high-confidence set (Alg. 1, phase 1).
+* :mod:`oracle.tree`       -- confidence-stratified tree construction (Alg. 1):
+  stratification, top-k expansion at the first level, top-1 deeper, pruning
+  by path confidence.
 * :mod:`oracle.brute`      -- scalar-loop re-derivations used only to pin the
   functions above on tiny inputs.
 
@@ -37,6 +40,7 @@ from .accept import (  # noqa: E402
     accept_batch,
     fragile_states,
 )
+from .tree import build_tree, build_tree_batch, gather_state_scores, level_widths  # noqa: E402
 
 __all__ = [
     "MASK",
@@ -49,4 +53,8 @@ __all__ = [
     "accept_sequence",
     "accept_batch",
     "fragile_states",
+    "build_tree",
+    "build_tree_batch",
+    "gather_state_scores",
+    "level_widths",
 ]
