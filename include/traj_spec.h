@@ -2,8 +2,8 @@
  * traj_spec.h -- C ABI of libtrajspec, the MI355X (gfx950) trajectory-verification step
  * for trajectory-level speculative decoding of diffusion language models.
  *
- * One verification step of the method (Sec. 3.1 overview, stage 3) runs three calls
- * back to back on one HIP stream:
+ * One verification step of the method (Sec. 3.1 overview, stage 3) runs calls 1-3 back
+ * to back on one HIP stream; call 4 (stage 2) builds the next step's drafts from its result:
  *   1. traj_verify_attn      -- attention of every draft block under the trajectory mask
  *                               (Sec. 3.3, "Attention masking for trajectory isolation").
  *   2. traj_confidence_topk  -- per-position confidence c(x) = max softmax and top-k
@@ -13,6 +13,9 @@
  *                               parent state and the greedy / longest-path walk
  *                               (Sec. 3.3, "Verification procedure"; Sec. 2.1 threshold
  *                               decoding; Alg. 1 phase 1 for the high-confidence set).
+ *   4. traj_build_tree       -- the next step's draft tree from the accepted state
+ *                               (Alg. 1: stratification, top-k first level, top-1 deeper,
+ *                               pruning by path confidence).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
@@ -53,7 +56,8 @@ typedef enum {
 typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
 
 /* Device status bits (traj_get_device_status). */
-#define TRAJ_DEV_BAD_PARENT 0x1 /* some parent[n] was outside [-1, n): treated as -1 */
+#define TRAJ_DEV_BAD_PARENT 0x1 /* some parent[n] was outside [-1, n): treated as -1      */
+#define TRAJ_DEV_BAD_LEAF 0x2   /* traj_build_tree: a leaf outside [-1, n_prev): taken as -1 */
 
 /* ------------------------------------------------------------------------------------
  * 1. Trajectory-masked verification attention  (Sec. 3.3; drafts packed as in Sec. 3.2
@@ -175,6 +179,63 @@ typedef struct {
 
 traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts* drafts,
                         float threshold, const traj_accepted* accepted, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * 4. Draft tree construction  (Alg. 1, confidence-stratified trajectory tree; Sec. 3.2
+ *    "Tree construction" and "Complexity analysis"; Sec. 3.1 logit reuse)
+ *
+ * Builds the next step's draft tree of every sequence from the state traj_accept accepted
+ * and the candidates the verification pass produced for that state:
+ *   s0        = state[b,:]                                   (traj_accept's out_tokens)
+ *   (C, I)    = conf[b, leaf[b]], idx[b, leaf[b]]   ([L,k])  when leaf[b] >= 0,
+ *               conf0[b], idx0[b]                            when leaf[b] == -1 or leaf == NULL.
+ * Phase 1: H = masked p with C[p,0] > threshold (strict), Low = masked p with
+ *   C[p,0] <= threshold.  The root is s0 with every p of H set to I[p,0]; when H is not
+ *   empty it is node 0 (parent -1), otherwise the root is s0 itself and is not emitted (the
+ *   first-level nodes then have parent -1).
+ * Phase 2, for levels l = 1 .. depth while Low has an l-th position q_l (Low ranked by
+ *   C[p,0], larger first, smaller p on equal values):
+ *   l = 1:  children j = 0 .. branch-1 of the root set q_1 to I[q_1, j]     (GenerateTopK);
+ *   l > 1:  each kept node of level l-1 gets one child setting q_l to I[q_l, 0] (GenerateTop1);
+ *   each level keeps its w_l best children by score (PruneByConfidence; generation order on
+ *   equal scores), w_l = max(width - l + 1, 1) (hybrid, full == 0) or width (full == 1).
+ *   score = sum of log C over the candidates chosen on the path below the root (root: 0),
+ *   accumulated in fp32 in path order.
+ *   With H empty, node 0 is one threshold-decoding step of s0 (the top-1 fallback), so an
+ *   exact-mode traj_accept of the tree always advances.
+ * Outputs (breadth first, each level in kept order; int32 unless stated):
+ *   tokens[b,n,:]   block state of node n, -1 = masked            [B, n_max, L]
+ *   parent[b,n]     -1 or the generating node's index (< n)       [B, n_max]
+ *   n_nodes[b]      number of nodes (0 when s0 has no masked position)  [B]
+ *   score[b,n]      float32 path log-confidence (may be NULL)      [B, n_max]
+ *   Slots n >= n_nodes[b] hold s0, parent -1 and score -inf: a copy of s0 is never a
+ *   consistent child, so the outputs can be verified and accepted as an n_max-draft tree.
+ *   conf_next / idx_next (float32 / int32 [B,L,k], may both be NULL): the gathered (C, I),
+ *   the committed-state candidates of the next traj_accept call (its conf0 / idx0).
+ * Each [k] candidate row must be non-increasing in confidence (as traj_confidence_topk
+ * writes it): the first level's pruning keeps candidates 0 .. w_1-1 on that basis.
+ * Limits: B >= 1; 1 <= L <= 64; 1 <= k <= 8; 1 <= branch <= k; width >= 1; depth >= 0;
+ *   n_prev >= 0 (drafts per sequence in conf / idx; both may be NULL when n_prev == 0 or
+ *   leaf == NULL); traj_tree_max_nodes(shape) <= n_max <= 64.
+ *   A leaf[b] outside [-1, n_prev) is taken as -1 and sets TRAJ_DEV_BAD_LEAF.
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    int32_t B, L, k;
+    int32_t n_prev;               /* drafts per sequence in conf / idx                 */
+    int32_t width, depth, branch; /* W, D and the candidates tried at the first level  */
+    int32_t full;                 /* 0 hybrid level widths, 1 full (width per level)   */
+    int32_t n_max;                /* node slots per sequence in the outputs            */
+} traj_tree_shape;
+
+/* Largest node count the shape's tree can reach (1 + sum over levels l <= min(depth, L) of
+ * c_l, c_1 = min(branch, w_1), c_l = min(w_l, c_{l-1})); -1 when the shape is invalid. */
+int32_t traj_tree_max_nodes(const traj_tree_shape* shape);
+
+traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const float* conf,
+                            const int32_t* idx, const float* conf0, const int32_t* idx0,
+                            const traj_tree_shape* shape, float threshold, int32_t* tokens,
+                            int32_t* parent, int32_t* n_nodes, float* score, float* conf_next,
+                            int32_t* idx_next, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Utilities

@@ -9,17 +9,25 @@ The three calls of one verification step (all HIP kernels in libtrajspec.so):
   candidates over the vocabulary.
 * :func:`accept`           -- threshold-decoding consistency and greedy /
   longest-path acceptance of the draft tree.
+
+and the next step's drafts:
+
+* :func:`build_tree`       -- confidence-stratified draft tree (Alg. 1) from the
+  accepted state and the candidates its verification produced.
 """
 
 from ._lib import (  # noqa: F401
+    DEV_BAD_LEAF,
     DEV_BAD_PARENT,
     LIB_PATH,
     TrajSpecError,
     accept,
+    build_tree,
     confidence_topk,
     confidence_topk_workspace_size,
     device_status,
     load,
+    tree_max_nodes,
     verify_attn,
     verify_attn_workspace_size,
     version,

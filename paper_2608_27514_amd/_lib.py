@@ -20,6 +20,7 @@ TRAJ_BF16, TRAJ_F32 = 0, 1
 MODES = {"exact": 0, "top1": 1, "topk": 2}
 TRAVERSALS = {"greedy": 0, "longest": 1}
 DEV_BAD_PARENT = 0x1
+DEV_BAD_LEAF = 0x2
 
 
 class TrajSpecError(RuntimeError):
@@ -51,6 +52,12 @@ class Accepted(ctypes.Structure):
                 ("out_tokens", ctypes.c_void_p), ("hi", ctypes.c_void_p)]
 
 
+class TreeShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("L", ctypes.c_int32), ("k", ctypes.c_int32), ("n_prev", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("depth", ctypes.c_int32), ("branch", ctypes.c_int32),
+                ("full", ctypes.c_int32), ("n_max", ctypes.c_int32)]
+
+
 _LIB = None
 
 EXPORTS = {
@@ -63,6 +70,9 @@ EXPORTS = {
                                               ctypes.c_void_p]),
     "traj_accept": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Drafts), ctypes.c_float,
                                      ctypes.POINTER(Accepted), ctypes.c_void_p]),
+    "traj_tree_max_nodes": (ctypes.c_int32, [ctypes.POINTER(TreeShape)]),
+    "traj_build_tree": (ctypes.c_int32, [ctypes.c_void_p] * 6 + [ctypes.POINTER(TreeShape), ctypes.c_float]
+                        + [ctypes.c_void_p] * 7),
     "traj_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "traj_version": (ctypes.c_char_p, []),
     "traj_get_device_status": (ctypes.c_int32, [ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_void_p]),
@@ -218,6 +228,58 @@ def accept(conf, idx, tokens, parent, committed, conf0, idx0, threshold, mode="e
     st = _lib().traj_accept(_ptr(conf), _ptr(idx), ctypes.byref(dr), float(threshold), ctypes.byref(ac),
                             _stream(stream))
     _check(st, "traj_accept")
+    return out
+
+
+# ---------------------------------------------------------------- tree construction
+def tree_shape(B, L, k, width, depth, branch, full=False, n_prev=0, n_max=None):
+    sh = TreeShape(B, L, k, n_prev, width, depth, branch, 1 if full else 0, 0)
+    if n_max is None:
+        n_max = int(_lib().traj_tree_max_nodes(ctypes.byref(sh)))
+        if n_max < 0:
+            raise ValueError("invalid tree shape")
+    sh.n_max = n_max
+    return sh
+
+
+def tree_max_nodes(B, L, k, width, depth, branch, full=False):
+    return int(_lib().traj_tree_max_nodes(ctypes.byref(tree_shape(B, L, k, width, depth, branch, full, n_max=0))))
+
+
+def build_tree(state, conf0, idx0, threshold, width, depth, branch, full=False, leaf=None, conf=None, idx=None,
+               n_max=None, out=None, stream=None):
+    """Next step's draft tree (Alg. 1) from the accepted state; returns a dict of device
+    tensors tokens [B,n_max,L], parent [B,n_max], n_nodes [B], score [B,n_max],
+    conf_next / idx_next [B,L,k].  With ``leaf`` (traj_accept's leaf) the candidates come
+    from conf/idx [B,N,L,k] (or [B*N*L,k]) of the verified tree, else from conf0/idx0."""
+    B, L = state.shape
+    k = conf0.shape[-1]
+    for name, t, dt in (("state", state, torch.int32), ("conf0", conf0, torch.float32), ("idx0", idx0, torch.int32)):
+        _dev(t, name, dt)
+    n_prev = 0
+    if leaf is not None:
+        _dev(leaf, "leaf", torch.int32)
+        _dev(conf, "conf", torch.float32)
+        _dev(idx, "idx", torch.int32)
+        n_prev = conf.numel() // (B * L * k)
+        if conf.numel() != B * n_prev * L * k or idx.numel() != conf.numel():
+            raise ValueError("conf/idx must hold B*N*L*k entries")
+    sh = tree_shape(B, L, k, width, depth, branch, full, n_prev, n_max)
+    dev = state.device
+    if out is None:
+        out = {
+            "tokens": torch.empty((B, sh.n_max, L), dtype=torch.int32, device=dev),
+            "parent": torch.empty((B, sh.n_max), dtype=torch.int32, device=dev),
+            "n_nodes": torch.empty(B, dtype=torch.int32, device=dev),
+            "score": torch.empty((B, sh.n_max), dtype=torch.float32, device=dev),
+            "conf_next": torch.empty((B, L, k), dtype=torch.float32, device=dev),
+            "idx_next": torch.empty((B, L, k), dtype=torch.int32, device=dev),
+        }
+    st = _lib().traj_build_tree(_ptr(state), _ptr(leaf), _ptr(conf), _ptr(idx), _ptr(conf0), _ptr(idx0),
+                                ctypes.byref(sh), float(threshold), _ptr(out["tokens"]), _ptr(out["parent"]),
+                                _ptr(out["n_nodes"]), _ptr(out.get("score")), _ptr(out.get("conf_next")),
+                                _ptr(out.get("idx_next")), _stream(stream))
+    _check(st, "traj_build_tree")
     return out
 
 

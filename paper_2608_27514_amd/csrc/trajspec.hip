@@ -9,6 +9,7 @@
 #include "accept.hpp"
 #include "common.hpp"
 #include "conf_topk.hpp"
+#include "tree.hpp"
 #include "verify_attn.hpp"
 
 namespace {
@@ -204,6 +205,63 @@ traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts
     p.traversal = drafts->traversal;
     p.tau = threshold;
     hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(kAcceptThreads), 0, as_stream(stream), p);
+    return launched();
+}
+
+int32_t traj_tree_max_nodes(const traj_tree_shape* sh) {
+    if (sh == nullptr || sh->B < 1 || sh->L < 1 || sh->L > kTreeMaxBlock || sh->k < 1 || sh->k > kTreeMaxK ||
+        sh->branch < 1 || sh->branch > sh->k || sh->width < 1 || sh->depth < 0 || sh->n_prev < 0 ||
+        (sh->full != 0 && sh->full != 1))
+        return -1;
+    int64_t total = 1, cnt = 0;
+    const int levels = sh->depth < sh->L ? sh->depth : sh->L;
+    for (int l = 1; l <= levels; ++l) {
+        const int64_t w = sh->full ? sh->width : (sh->width - l + 1 > 1 ? sh->width - l + 1 : 1);
+        cnt = l == 1 ? (sh->branch < w ? sh->branch : w) : (w < cnt ? w : cnt);
+        total += cnt;
+    }
+    return (int32_t)total;
+}
+
+traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const float* conf, const int32_t* idx,
+                            const float* conf0, const int32_t* idx0, const traj_tree_shape* shape, float threshold,
+                            int32_t* tokens, int32_t* parent, int32_t* n_nodes, float* score, float* conf_next,
+                            int32_t* idx_next, void* stream) {
+    if (shape == nullptr || state == nullptr || conf0 == nullptr || idx0 == nullptr || tokens == nullptr ||
+        parent == nullptr || n_nodes == nullptr)
+        return TRAJ_E_NULL;
+    if (leaf != nullptr && shape->n_prev > 0 && (conf == nullptr || idx == nullptr)) return TRAJ_E_NULL;
+    if ((conf_next == nullptr) != (idx_next == nullptr)) return TRAJ_E_NULL;
+    if (shape->k < 1 || shape->k > kTreeMaxK || shape->branch < 1 || shape->branch > shape->k ||
+        (shape->full != 0 && shape->full != 1))
+        return TRAJ_E_ARG;
+    if (!(threshold == threshold)) return TRAJ_E_ARG;
+    const int32_t need = traj_tree_max_nodes(shape);
+    if (need < 0 || shape->n_max < need || shape->n_max > kTreeMaxBlock) return TRAJ_E_SHAPE;
+    TreeParams p{};
+    p.state = state;
+    p.leaf = leaf;
+    p.conf = conf;
+    p.idx = idx;
+    p.conf0 = conf0;
+    p.idx0 = idx0;
+    p.tokens = tokens;
+    p.parent = parent;
+    p.n_nodes = n_nodes;
+    p.score = score;
+    p.conf_next = conf_next;
+    p.idx_next = idx_next;
+    p.B = shape->B;
+    p.L = shape->L;
+    p.k = shape->k;
+    p.n_prev = leaf != nullptr ? shape->n_prev : 0;
+    p.width = shape->width;
+    p.depth = shape->depth;
+    p.branch = shape->branch;
+    p.full = shape->full;
+    p.n_max = shape->n_max;
+    p.tau = threshold;
+    hipLaunchKernelGGL(build_tree_kernel, dim3(p.B), dim3(kTreeThreads), 0, as_stream(stream), p);
     return launched();
 }
 

@@ -38,7 +38,7 @@ def random_state(rng, L, k, p_mask=0.7, tau=0.9, ties=False):
         top = np.round(top * 4) / 4  # many equal confidences
     conf = np.zeros((L, k), dtype=np.float32)
     for p in range(L):
-        rest = np.sort(rng.random(k - 1))[::-1] * (1 - top[p]) / max(k - 1, 1)
+        rest = np.minimum(np.sort(rng.random(k - 1))[::-1] * (1 - top[p]) / max(k - 1, 1), top[p])
         conf[p] = np.concatenate([[top[p]], rest]).astype(np.float32)
     idx = np.stack([rng.permutation(1000)[:k] for _ in range(L)])
     return s0, conf, idx
