@@ -208,6 +208,31 @@ def cpu_baseline(x, buf, wl, tau, n_seq):
     }
 
 
+TREE_WIDTH, TREE_DEPTH = 3, 3  # the paper's adopted W3D3 hybrid tree
+
+
+def time_tree_build(x, buf, tau, stream, reps=50):
+    """The next step's drafts from this step's acceptance (traj_build_tree, Alg. 1), timed
+    with HIP events on the launch stream; not part of the verification step above."""
+    wl = x.wl
+    k = wl.k
+    conf = buf.conf.view(wl.B, wl.N, wl.L, k)
+    idx = buf.idx.view(wl.B, wl.N, wl.L, k)
+    args = (buf.acc["out_tokens"], x.conf0, x.idx0, tau, TREE_WIDTH, TREE_DEPTH, k)
+    kw = dict(leaf=buf.acc["leaf"], conf=conf, idx=idx, stream=stream)
+    out = tsp.build_tree(*args, **kw)
+    kw["out"] = out
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        tsp.build_tree(*args, **kw)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    n_nodes = out["n_nodes"].cpu().numpy()
+    return {"ms": e0.elapsed_time(e1) / reps, "tree": f"W{TREE_WIDTH}D{TREE_DEPTH} hybrid, branch {k}",
+            "node_slots": int(out["parent"].shape[1]), "mean_nodes": float(n_nodes.mean())}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,6 +307,7 @@ def main():
     run_step(x, buf, tau, stream)
     torch.cuda.synchronize()
     acc_main = buf.acc["n_accepted"].cpu().numpy()
+    tree = time_tree_build(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
     result = {
@@ -322,6 +348,7 @@ def main():
         "attention_hbm_bytes_per_launch": attn_bytes(wl),
         "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
         "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},
+        "tree_build": tree,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:
