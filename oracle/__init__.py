@@ -15,6 +15,8 @@ Decoding for Diffusion LLMs):
 * :mod:`oracle.tree`       -- confidence-stratified tree construction (Alg. 1):
   stratification, top-k expansion at the first level, top-1 deeper, pruning
   by path confidence.
+* :mod:`oracle.interblock` -- inter-block speculation trigger and the joint
+  tree's root-to-root visibility (Sec. 3.4, App. D).
 * :mod:`oracle.brute`      -- scalar-loop re-derivations used only to pin the
   functions above on tiny inputs.
 
@@ -31,7 +33,7 @@ invariants, hand-worked fixtures (``tests/golden/``) or brute force.
 
 MASK = -1  # token id used for a still-masked position in block states
 
-from .attention import ancestor_sets, trajectory_mask, verify_attention  # noqa: E402
+from .attention import ancestor_sets, trajectory_mask, verify_attention, visible_sets  # noqa: E402
 from .confidence import confidence_topk  # noqa: E402
 from .accept import (  # noqa: E402
     threshold_step,
@@ -41,6 +43,7 @@ from .accept import (  # noqa: E402
     fragile_states,
 )
 from .tree import build_tree, build_tree_batch, gather_state_scores, level_widths  # noqa: E402
+from .interblock import block_top1_confidence, interblock_trigger, interblock_trigger_batch, joint_peers  # noqa: E402
 
 __all__ = [
     "MASK",
@@ -57,4 +60,9 @@ __all__ = [
     "build_tree_batch",
     "gather_state_scores",
     "level_widths",
+    "visible_sets",
+    "block_top1_confidence",
+    "interblock_trigger",
+    "interblock_trigger_batch",
+    "joint_peers",
 ]

@@ -18,6 +18,12 @@ masking for trajectory isolation; Sec. 3.2 / Alg. 1 for the draft tree):
 * Softmax scale defaults to 1/sqrt(D) (the paper does not state one).
 * Grouped-query attention: query head ``h`` reads K/V head ``h // (Hq // Hkv)``
   (heads of one group are contiguous).
+* Inter-block speculation (Sec. 3.4 "Joint tree construction", App. D) verifies
+  the trees of two consecutive blocks in one pass and keeps the roots of the two
+  blocks visible to each other's drafts.  That visibility is not a parent
+  relation, so it comes in as ``peers``: bit j of ``peers[b, n]`` makes every
+  token of draft j visible to draft n on top of its root path (one direction;
+  symmetric visibility sets both bits).
 
 Layouts (all row-major):
   q        [B, N, L, Hq, D]
@@ -61,24 +67,35 @@ def ancestor_sets(parent_row):
     return out
 
 
-def trajectory_mask(parent_row, L, S):
+def visible_sets(parent_row, peers_row=None):
+    """anc*(i) plus the drafts whose bits are set in peers_row[i] (bits >= N ignored)."""
+    vis = ancestor_sets(parent_row)
+    if peers_row is not None:
+        n_drafts = len(parent_row)
+        for i in range(n_drafts):
+            bits = int(peers_row[i]) & ((1 << 64) - 1)
+            vis[i] |= {j for j in range(n_drafts) if (bits >> j) & 1}
+    return vis
+
+
+def trajectory_mask(parent_row, L, S, peers_row=None):
     """Dense boolean visibility mask of shape [N*L, S + N*L].
 
     Row ``i*L + p`` is query token p of draft i.  Column ``s < S`` is cache
     token s (always visible); column ``S + j*L + p'`` is token p' of draft j,
-    visible iff j is in anc*(i).
+    visible iff j is in anc*(i) or bit j of peers_row[i] is set.
     """
-    anc = ancestor_sets(parent_row)
+    vis = visible_sets(parent_row, peers_row)
     n_drafts = len(parent_row)
     mask = np.zeros((n_drafts * L, S + n_drafts * L), dtype=bool)
     mask[:, :S] = True
     for i in range(n_drafts):
-        for j in anc[i]:
+        for j in vis[i]:
             mask[i * L:(i + 1) * L, S + j * L:S + (j + 1) * L] = True
     return mask
 
 
-def verify_attention(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None):
+def verify_attention(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None, peers=None):
     """Trajectory-masked attention for every draft token, fp64.
 
     Per (sequence b, query head h): build K_all = [cache keys; all draft keys
@@ -109,7 +126,7 @@ def verify_attention(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None):
 
     out = np.zeros((B, N, L, Hq, D), dtype=np.float64)
     for b in range(B):
-        mask = trajectory_mask(parent[b], L, S)
+        mask = trajectory_mask(parent[b], L, S, None if peers is None else peers[b])
         for h in range(Hq):
             g = h // group
             q_h = q[b, :, :, h, :].reshape(N * L, D)

@@ -30,7 +30,7 @@ def _is_on_root_path(j, i, parent_row):
     return False
 
 
-def attention_scalar(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None):
+def attention_scalar(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None, peers=None):
     """Nested-loop attention.  Arrays are nested sequences or numpy arrays with
     the layouts of :func:`oracle.attention.verify_attention`."""
     B = len(q)
@@ -56,7 +56,8 @@ def attention_scalar(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None):
                         keys.append(k_cache[b][s][g])
                         vals.append(v_cache[b][s][g])
                     for j in range(N):
-                        if _is_on_root_path(j, i, parent[b]):
+                        extra = peers is not None and (int(peers[b][i]) >> j) & 1
+                        if _is_on_root_path(j, i, parent[b]) or extra:
                             for pp in range(L):
                                 keys.append(k_draft[b][j][pp][g])
                                 vals.append(v_draft[b][j][pp][g])
