@@ -16,6 +16,9 @@
  *   4. traj_build_tree       -- the next step's draft tree from the accepted state
  *                               (Alg. 1: stratification, top-k first level, top-1 deeper,
  *                               pruning by path confidence).
+ *   5. traj_interblock_trigger and traj_verify_attn_peers -- inter-block speculation
+ *                               (Sec. 3.4): the trigger, and attention for the joint trees of
+ *                               two blocks with root-to-root visibility.
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
@@ -99,6 +102,19 @@ traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_c
                              const int32_t* draft_parent, void* out,
                              const traj_attn_shape* shape,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* traj_verify_attn with per-draft peer visibility  (Sec. 3.4 "Joint tree construction",
+ * App. D: when the trees of blocks B_t and B_{t+1} are verified in one pass, draft tokens of
+ * B_{t+1} attend to the root of B_t and vice versa).
+ * draft_peers [B, N] uint64 (device, may be NULL = traj_verify_attn): bit j of
+ * draft_peers[b,n] makes all L tokens of draft j visible to draft n in addition to the cache,
+ * itself and its ancestors; one direction per bit (mutual visibility sets both); bits >= N
+ * are ignored.  Everything else as traj_verify_attn. */
+traj_status traj_verify_attn_peers(const void* q, const void* k_cache, const void* v_cache,
+                                   const void* k_draft, const void* v_draft,
+                                   const int32_t* draft_parent, const uint64_t* draft_peers,
+                                   void* out, const traj_attn_shape* shape,
+                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * 2. Confidence and top-k candidates  (Sec. 3.2, Eq. 2; "Candidate collection")
@@ -236,6 +252,24 @@ traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const flo
                             const traj_tree_shape* shape, float threshold, int32_t* tokens,
                             int32_t* parent, int32_t* n_nodes, float* score, float* conf_next,
                             int32_t* idx_next, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * 5. Inter-block speculation trigger  (Sec. 3.4 "Trigger condition", App. D)
+ *
+ * For every sequence b, with the states and candidates of two consecutive blocks packed as
+ * 2L positions (B_t at 0..L-1, B_{t+1} at L..2L-1; one verification pass whose drafts cover
+ * both blocks produces them):
+ *   c_cur[b]  = max of conf[b,p,0] over masked p < L           (0 when none is masked)
+ *   c_next[b] = max of conf[b,p,0] over masked L <= p < 2L     (0 when none is masked)
+ *   trigger[b] = 1 iff B_{t+1} has a masked position and (c_next > c_cur or c_next > threshold),
+ * in fp32, strict comparisons.
+ * state [B, 2L] int32 (-1 = masked), conf [B, 2L, k] float32 (traj_confidence_topk's rows),
+ * trigger [B] uint8, c_cur / c_next [B] float32 (each may be NULL).
+ * Limits: B >= 1; 1 <= L <= 64; 1 <= k <= 8.
+ * ------------------------------------------------------------------------------------ */
+traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int32_t B, int32_t L,
+                                    int32_t k, float threshold, uint8_t* trigger, float* c_cur,
+                                    float* c_next, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Utilities

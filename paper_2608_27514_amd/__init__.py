@@ -14,6 +14,12 @@ and the next step's drafts:
 
 * :func:`build_tree`       -- confidence-stratified draft tree (Alg. 1) from the
   accepted state and the candidates its verification produced.
+
+and inter-block speculation (Sec. 3.4):
+
+* :func:`interblock_trigger` -- whether the next block is confident enough to
+  speculate on both blocks; :func:`verify_attn` with ``peers`` (see
+  :func:`joint_peers`) verifies the joint trees with root-to-root visibility.
 """
 
 from ._lib import (  # noqa: F401
@@ -26,6 +32,8 @@ from ._lib import (  # noqa: F401
     confidence_topk,
     confidence_topk_workspace_size,
     device_status,
+    interblock_trigger,
+    joint_peers,
     load,
     tree_max_nodes,
     verify_attn,

@@ -8,6 +8,8 @@ If the library is not built the calls raise -- there is no fallback.
 import ctypes
 import os
 
+import numpy as np
+
 import torch
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -70,6 +72,11 @@ EXPORTS = {
                                               ctypes.c_void_p]),
     "traj_accept": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Drafts), ctypes.c_float,
                                      ctypes.POINTER(Accepted), ctypes.c_void_p]),
+    "traj_verify_attn_peers": (ctypes.c_int32, [ctypes.c_void_p] * 8 + [ctypes.POINTER(AttnShape), ctypes.c_void_p,
+                                                                         ctypes.c_size_t, ctypes.c_void_p]),
+    "traj_interblock_trigger": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                                 ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_void_p, ctypes.c_void_p]),
     "traj_tree_max_nodes": (ctypes.c_int32, [ctypes.POINTER(TreeShape)]),
     "traj_build_tree": (ctypes.c_int32, [ctypes.c_void_p] * 6 + [ctypes.POINTER(TreeShape), ctypes.c_float]
                         + [ctypes.c_void_p] * 7),
@@ -140,21 +147,69 @@ def verify_attn_workspace_size(shape):
 
 
 def verify_attn(q, k_cache, v_cache, k_draft, v_draft, draft_parent, out=None, scale=0.0, workspace=None,
-                stream=None):
-    """Trajectory-masked attention; returns ``out`` [B,N,L,Hq,D] bf16."""
+                stream=None, peers=None):
+    """Trajectory-masked attention; returns ``out`` [B,N,L,Hq,D] bf16.  ``peers`` ([B,N]
+    int64 holding uint64 bit masks) adds visible drafts per draft (traj_verify_attn_peers)."""
     for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("k_draft", k_draft),
                     ("v_draft", v_draft)):
         _dev(t, name, torch.bfloat16)
     _dev(draft_parent, "draft_parent", torch.int32)
+    if peers is not None:
+        _dev(peers, "peers", torch.int64)
+        if tuple(peers.shape) != tuple(draft_parent.shape):
+            raise ValueError("peers must be [B,N] like draft_parent")
     if out is None:
         out = torch.empty_like(q)
     _dev(out, "out", torch.bfloat16)
     shape = attn_shape(q, k_cache, scale)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    st = _lib().traj_verify_attn(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_draft), _ptr(v_draft),
-                                 _ptr(draft_parent), _ptr(out), ctypes.byref(shape), _ptr(workspace),
-                                 ws_bytes, _stream(stream))
-    _check(st, "traj_verify_attn")
+    if peers is None:
+        st = _lib().traj_verify_attn(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_draft), _ptr(v_draft),
+                                     _ptr(draft_parent), _ptr(out), ctypes.byref(shape), _ptr(workspace),
+                                     ws_bytes, _stream(stream))
+        _check(st, "traj_verify_attn")
+    else:
+        st = _lib().traj_verify_attn_peers(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_draft), _ptr(v_draft),
+                                           _ptr(draft_parent), _ptr(peers), _ptr(out), ctypes.byref(shape),
+                                           _ptr(workspace), ws_bytes, _stream(stream))
+        _check(st, "traj_verify_attn_peers")
+    return out
+
+
+def joint_peers(n_cur, n_next, root_cur=0, root_next=0):
+    """Host-side peer masks for the joint trees of two blocks packed as drafts
+    [0, n_cur) (block t) and [n_cur, n_cur + n_next) (block t+1): every draft of block t+1
+    sees block t's root draft and every draft of block t sees block t+1's root draft.
+    Returns a [n_cur + n_next] int64 CPU tensor holding the uint64 bit masks."""
+    n = n_cur + n_next
+    if not (0 <= root_cur < n_cur and 0 <= root_next < n_next and n <= 64):
+        raise ValueError("roots must index their trees and n_cur + n_next <= 64")
+    bits = np.zeros(n, dtype=np.uint64)
+    bits[:n_cur] |= np.uint64(1) << np.uint64(n_cur + root_next)
+    bits[n_cur:] |= np.uint64(1) << np.uint64(root_cur)
+    return torch.from_numpy(bits.view(np.int64).copy())
+
+
+def interblock_trigger(state, conf, threshold, out=None, stream=None):
+    """Inter-block trigger per sequence from state [B,2L] int32 and conf [B,2L,k] (or
+    [B*2L,k]) float32; returns dict trigger [B] uint8, c_cur [B], c_next [B] float32."""
+    B, L2 = state.shape
+    if L2 % 2:
+        raise ValueError("state must hold two blocks (2L positions) per sequence")
+    k = conf.numel() // (B * L2)
+    if conf.numel() != B * L2 * k:
+        raise ValueError("conf must hold B*2L*k entries")
+    _dev(state, "state", torch.int32)
+    _dev(conf, "conf", torch.float32)
+    dev = state.device
+    if out is None:
+        out = {"trigger": torch.empty(B, dtype=torch.uint8, device=dev),
+               "c_cur": torch.empty(B, dtype=torch.float32, device=dev),
+               "c_next": torch.empty(B, dtype=torch.float32, device=dev)}
+    st = _lib().traj_interblock_trigger(_ptr(state), _ptr(conf), B, L2 // 2, k, float(threshold),
+                                        _ptr(out["trigger"]), _ptr(out.get("c_cur")), _ptr(out.get("c_next")),
+                                        _stream(stream))
+    _check(st, "traj_interblock_trigger")
     return out
 
 

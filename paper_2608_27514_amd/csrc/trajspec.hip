@@ -9,6 +9,7 @@
 #include "accept.hpp"
 #include "common.hpp"
 #include "conf_topk.hpp"
+#include "interblock.hpp"
 #include "tree.hpp"
 #include "verify_attn.hpp"
 
@@ -107,6 +108,14 @@ size_t traj_verify_attn_workspace_size(const traj_attn_shape* shape) {
 traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_cache, const void* k_draft,
                              const void* v_draft, const int32_t* draft_parent, void* out,
                              const traj_attn_shape* shape, void* workspace, size_t workspace_bytes, void* stream) {
+    return traj_verify_attn_peers(q, k_cache, v_cache, k_draft, v_draft, draft_parent, nullptr, out, shape,
+                                  workspace, workspace_bytes, stream);
+}
+
+traj_status traj_verify_attn_peers(const void* q, const void* k_cache, const void* v_cache, const void* k_draft,
+                                   const void* v_draft, const int32_t* draft_parent, const uint64_t* draft_peers,
+                                   void* out, const traj_attn_shape* shape, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
     (void)workspace;
     (void)workspace_bytes;
     if (shape == nullptr || q == nullptr || k_draft == nullptr || v_draft == nullptr || draft_parent == nullptr ||
@@ -126,6 +135,7 @@ traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_c
     p.kd = static_cast<const uint16_t*>(k_draft);
     p.vd = static_cast<const uint16_t*>(v_draft);
     p.parent = draft_parent;
+    p.peers = draft_peers;
     p.out = static_cast<uint16_t*>(out);
     p.B = shape->B;
     p.N = shape->N;
@@ -205,6 +215,16 @@ traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts
     p.traversal = drafts->traversal;
     p.tau = threshold;
     hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(kAcceptThreads), 0, as_stream(stream), p);
+    return launched();
+}
+
+traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int32_t B, int32_t L, int32_t k,
+                                    float threshold, uint8_t* trigger, float* c_cur, float* c_next, void* stream) {
+    if (state == nullptr || conf == nullptr || trigger == nullptr) return TRAJ_E_NULL;
+    if (B < 1 || L < 1 || L > kTriggerMaxBlock) return TRAJ_E_SHAPE;
+    if (k < 1 || k > 8 || !(threshold == threshold)) return TRAJ_E_ARG;
+    TriggerParams p{state, conf, trigger, c_cur, c_next, B, L, k, threshold};
+    hipLaunchKernelGGL(interblock_trigger_kernel, dim3(B), dim3(64), 0, as_stream(stream), p);
     return launched();
 }
 

@@ -27,21 +27,23 @@
 //   swizzle puts in its slot.  Draft tiles use global_load_lds_dwordx4 the same way.
 //
 // Phases per workgroup
-//   0. prologue: the parent array, Q, the K rows of cache block 0 and the first stage are all
-//      requested before anything waits; wave 0 builds the 64-bit ancestor masks from the
+//   0. prologue: the parent array, Q, the K rows of cache keys 0..63 and the first stage are
+//      all requested before anything waits; wave 0 builds the 64-bit ancestor masks from the
 //      parent array with lane shuffles.
-//   1. cache, software-pipelined per 32-key block: the body of block j issues the score
-//      chain of block j+1 on the matrix cores, computes block j's weights on the vector
-//      ALUs in between, then O += V_j P_j.  Stage t holds the K rows of blocks 2t+1, 2t+2 and
-//      the V rows of blocks 2t, 2t+1 in one of two LDS buffers (separate arrays, so the
-//      compiler can see that the direct loads into one never alias reads of the other);
-//      the next stage is loaded while the current one is computed, one barrier per stage.
-//      Stage pairs whose successors are full run with no conditional code; the last stages
-//      take per-block checks for the partial block.
+//   1. cache, in 64-key steps: a softmax phase turns the scores of two 32-key blocks into
+//      bf16 weights on the vector ALUs, then a matrix phase computes the scores of the next two
+//      blocks and adds the weighted V rows of the current two (32 MFMAs back to back).  Two
+//      waves of different workgroups share each SIMD, so one's softmax phase overlaps the
+//      other's matrix phase.  Stage t holds the V rows of blocks 2t, 2t+1 and the K rows of
+//      blocks 2t+2, 2t+3 in one of two LDS buffers (separate arrays, so the compiler can see
+//      that the direct loads into one never alias reads of the other); the next stage loads
+//      during the current step, one barrier per step.  Step pairs whose next stages are full
+//      run with no conditional code; the last steps mask the scores of keys past S.
 //   2. drafts: each wave visits only the 32-key tiles holding its own block or an ancestor
-//      block (the set bits of the OR of its rows' ancestor masks, lowest first).  Tiles
-//      that hold only fully visible blocks need no per-element mask (always the case when
-//      L is a multiple of 32 and a wave's rows share a draft).
+//      block (the set bits of the OR of its rows' ancestor masks, lowest first); optional
+//      per-draft peer masks add drafts to a draft's visible set (inter-block speculation).
+//      Tiles that hold only fully visible blocks need no per-element mask (always the case
+//      when L is a multiple of 32 and a wave's rows share a draft).
 #pragma once
 
 #include "common.hpp"
@@ -55,6 +57,7 @@ struct AttnParams {
     const uint16_t* kd;
     const uint16_t* vd;
     const int32_t* parent;
+    const uint64_t* peers;  // [B,N] extra visible drafts per draft (bit j = draft j), or null
     uint16_t* out;
     int B, N, L, Hq, Hkv, S;
     int group;           // Hq / Hkv
@@ -426,6 +429,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     // The parent array (ancestor walk below) is loaded first: the walk then waits for this
     // load only, not for the Q, K and stage loads issued after it.
     const int pj = (wave == 0 && lane < N) ? P.parent[(int64_t)b * N + lane] : -1;
+    const uint64_t peer_bits = (P.peers != nullptr && wave == 0 && lane < N) ? P.peers[(int64_t)b * N + lane] : 0ull;
 
     // This lane's query row (lanes l and l^32 share a row).
     const int row = (wg_in_group * kAttnWaves + wave) * 32 + (lane & 31);
@@ -534,7 +538,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
             j = go ? nj : -1;
             live = go;
         }
-        if (lane < N) anc[lane] = msk;
+        // drafts made visible beyond the root path (the joint trees of inter-block
+        // speculation), restricted to the N drafts of the sequence
+        const uint64_t in_range = N == 64 ? ~0ull : ((1ull << N) - 1ull);
+        if (lane < N) anc[lane] = msk | (peer_bits & in_range);
     }
     if (nb > 0) {
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);

@@ -161,3 +161,33 @@ def test_tree_argument_errors_and_max_nodes():
             total += cnt
         sh = shape(width=W, depth=D, branch=br, full=full, L=L, k=8)
         assert lib.traj_tree_max_nodes(ctypes.byref(sh)) == total
+
+
+@needs_lib
+def test_interblock_argument_errors():
+    lib = _lib.load()
+    sh = _lib.AttnShape(1, 4, 8, 4, 4, 64, 192, 0.0)
+    p7 = [FAKE] * 6
+    assert lib.traj_verify_attn_peers(*p7, None, None, ctypes.byref(sh), None, 0, None) == 1   # out NULL
+    assert lib.traj_verify_attn_peers(None, *([FAKE] * 5), None, FAKE, ctypes.byref(sh), None, 0, None) == 1
+    bad = _lib.AttnShape(1, 65, 8, 4, 4, 64, 192, 0.0)
+    assert lib.traj_verify_attn_peers(*p7, FAKE, FAKE, ctypes.byref(bad), None, 0, None) == 2
+
+    def trig(state=FAKE, conf=FAKE, B=2, L=8, k=3, tau=0.9, out=FAKE):
+        return lib.traj_interblock_trigger(state, conf, B, L, k, tau, out, None, None, None)
+
+    assert trig(state=None) == 1 and trig(conf=None) == 1 and trig(out=None) == 1
+    assert trig(B=0) == 2 and trig(L=0) == 2 and trig(L=65) == 2
+    assert trig(k=0) == 7 and trig(k=9) == 7 and trig(tau=float("nan")) == 7
+
+
+def test_joint_peers_helper_matches_oracle():
+    import numpy as np
+
+    from oracle.interblock import joint_peers as ref
+
+    for n_cur, n_next, rc, rn in [(3, 2, 0, 0), (7, 4, 0, 1), (60, 4, 2, 3), (1, 63, 0, 62)]:
+        got = _lib.joint_peers(n_cur, n_next, rc, rn).numpy().view(np.uint64)
+        assert [int(x) for x in got] == ref(n_cur, n_next, rc, rn)
+    with pytest.raises(ValueError):
+        _lib.joint_peers(60, 5)
