@@ -233,6 +233,44 @@ def time_tree_build(x, buf, tau, stream, reps=50):
             "node_slots": int(out["parent"].shape[1]), "mean_nodes": float(n_nodes.mean())}
 
 
+def time_interblock(x, buf, tau, stream, reps=5, trig_reps=50):
+    """Inter-block speculation pieces on the same inputs (not part of the step): attention with
+    root-to-root peer visibility for a joint packing (the last drafts form the next block's tree,
+    the first draft of each tree is its root), and the trigger on two blocks' states."""
+    wl = x.wl
+    n_next = min(4, wl.N - 1)
+    if n_next < 1:
+        return None
+    peers = tsp.joint_peers(wl.N - n_next, n_next).to(x.q.device).repeat(wl.B, 1).contiguous()
+    scratch = torch.empty_like(buf.out)  # buf.out stays the step's output
+    times = {"plain": 0.0, "peers": 0.0}
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2 * reps)]
+    for r in range(2 * reps + 2):  # alternate the two variants; the first pair warms up
+        name = "plain" if r % 2 == 0 else "peers"
+        kw = dict(out=scratch, stream=stream, peers=peers if name == "peers" else None)
+        if r >= 2:
+            evs[r - 2][0].record(stream)
+        tsp.verify_attn(x.q, x.kc, x.vc, x.kd, x.vd, x.parent, **kw)
+        if r >= 2:
+            evs[r - 2][1].record(stream)
+    torch.cuda.synchronize()
+    for r in range(2 * reps):
+        times["plain" if r % 2 == 0 else "peers"] += evs[r][0].elapsed_time(evs[r][1]) / reps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # trigger: the accepted block state followed by the committed state as the next block
+    state2 = torch.cat([buf.acc["out_tokens"], x.committed], 1).contiguous()
+    conf2 = buf.conf.view(wl.B, wl.N * wl.L, wl.k)[:, :2 * wl.L].contiguous()
+    out = tsp.interblock_trigger(state2, conf2, tau, stream=stream)
+    e0.record(stream)
+    for _ in range(trig_reps):
+        tsp.interblock_trigger(state2, conf2, tau, out=out, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return {"joint_drafts": f"{wl.N - n_next}+{n_next}, root-to-root peers", "attn_peers_ms": times["peers"],
+            "attn_plain_ms": times["plain"], "trigger_ms": e0.elapsed_time(e1) / trig_reps,
+            "triggered_sequences": int(out["trigger"].sum().item())}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -308,6 +346,7 @@ def main():
     torch.cuda.synchronize()
     acc_main = buf.acc["n_accepted"].cpu().numpy()
     tree = time_tree_build(x, buf, tau, stream)
+    inter = time_interblock(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
     result = {
@@ -349,6 +388,7 @@ def main():
         "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
         "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},
         "tree_build": tree,
+        "interblock": inter,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:
