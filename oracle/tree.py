@@ -20,7 +20,9 @@ taken here are:
 * GenerateTopK(n, Low, k): ``branch`` children; child j sets the candidate position to its
   j-th candidate token.  With H empty, child 0 is exactly one threshold-decoding step of s0
   (the top-1 fallback), so an exact-mode acceptance can always advance.
-* GenerateTop1(n, Low): one child setting the candidate position to its top-1 token.
+* GenerateTop1(n, Low): one child setting the candidate position to its top-1 token.  The
+  expansion ablation (App. C, "full top-2") expands every level with the top 2: ``branch_deep``
+  children per node below the first level (1 = the hybrid policy).
 * A node's score: the sum of log conf of the candidates chosen on its path below the root
   (root 0).  PruneByConfidence(frontier, w) keeps the w highest scores, ties to generation
   order.
@@ -53,7 +55,7 @@ def _candidate_position(state, low, conf):
     return min(cands, key=lambda p: _rank_key(p, conf))
 
 
-def build_tree(s0, conf, idx, tau, width, depth, branch, full=False):
+def build_tree(s0, conf, idx, tau, width, depth, branch, full=False, branch_deep=1):
     """Builds the draft tree for one sequence.
 
     s0: [L] block state (MASK = -1); conf/idx: [L,k] top-k confidences / candidates at s0.
@@ -62,8 +64,8 @@ def build_tree(s0, conf, idx, tau, width, depth, branch, full=False):
     s0 = np.asarray(s0)
     L = len(s0)
     k = len(idx[0]) if L else 0
-    if not 1 <= branch <= max(k, 1):
-        raise ValueError("branch must be in 1..k")
+    if not 1 <= branch <= max(k, 1) or not 1 <= branch_deep <= max(k, 1):
+        raise ValueError("branch and branch_deep must be in 1..k")
     # Phase 1: confidence stratification
     masked = [p for p in range(L) if s0[p] == MASK]
     high = [p for p in masked if conf[p][0] > tau]
@@ -91,7 +93,7 @@ def build_tree(s0, conf, idx, tau, width, depth, branch, full=False):
             p = _candidate_position(state, low, conf)
             if p is None:
                 continue
-            n_children = branch if level == 1 else 1  # GenerateTopK at the root, GenerateTop1 deeper
+            n_children = branch if level == 1 else branch_deep  # GenerateTopK at the root, GenerateTop1 deeper
             for j in range(n_children):
                 child = state.copy()
                 child[p] = idx[p][j]
@@ -123,7 +125,7 @@ def gather_state_scores(leaf, conf, idx, conf0, idx0):
     return np.asarray(conf0), np.asarray(idx0)
 
 
-def build_tree_batch(state, leaf, conf, idx, conf0, idx0, tau, width, depth, branch, full, n_max):
+def build_tree_batch(state, leaf, conf, idx, conf0, idx0, tau, width, depth, branch, full, n_max, branch_deep=1):
     """Batched form with the library's output layout: tokens [B,n_max,L], parent [B,n_max],
     n_nodes [B], score [B,n_max]; slots past n_nodes hold the state itself, parent -1,
     score -inf (a copy of the state is never a consistent child)."""
@@ -137,7 +139,7 @@ def build_tree_batch(state, leaf, conf, idx, conf0, idx0, tau, width, depth, bra
         lf = int(leaf[b]) if leaf is not None else -1
         C, I = gather_state_scores(lf, None if conf is None else conf[b], None if idx is None else idx[b],
                                    conf0[b], idx0[b])
-        t, p, s = build_tree(state[b], C, I, tau, width, depth, branch, full)
+        t, p, s = build_tree(state[b], C, I, tau, width, depth, branch, full, branch_deep)
         n = len(p)
         if n > n_max:
             raise ValueError("tree larger than n_max")

@@ -23,7 +23,7 @@ def test_golden_trees(case):
     conf = np.array(case["conf"], dtype=np.float32)
     idx = np.array(case["idx"])
     tokens, parent, score = build_tree(case["s0"], conf, idx, case["tau"], case["width"], case["depth"],
-                                       case["branch"], bool(case["full"]))
+                                       case["branch"], bool(case["full"]), case.get("branch_deep", 1))
     L = len(case["s0"])
     assert tokens.tolist() == [list(r) for r in np.array(case["tokens"], dtype=np.int64).reshape(-1, L)]
     assert parent.tolist() == case["parent"]
@@ -190,3 +190,38 @@ def test_gather_uses_leaf_rows():
     t_c, _, n_c, _ = build_tree_batch(s0[None], np.array([-1]), conf, idx, c[None], i[None], 0.9, 2, 2, 2, False, 8)
     t_ref, p_ref, _ = build_tree(s0, c, i, 0.9, 2, 2, 2, False)
     assert n_c[0] == len(p_ref) and np.array_equal(t_c[0, :len(p_ref)], t_ref)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_deeper_branching_prunes_to_the_best(seed):
+    """With several children per node below the first level (the ablation's top-2 policy), each
+    level holds the w_l best children of the kept nodes of the level above: none of the
+    children left out scores higher than a kept one, and kept nodes come best first."""
+    rng = np.random.default_rng(300 + seed)
+    L, k, tau = 10, 4, 0.9
+    s0, conf, idx = random_state(rng, L, k, tau=tau, ties=seed % 4 == 0)
+    W, D, bd = int(rng.integers(1, 5)), int(rng.integers(1, 5)), int(rng.integers(2, k + 1))
+    full = bool(seed % 2)
+    tokens, parent, score = build_tree(s0, conf, idx, tau, W, D, int(rng.integers(1, k + 1)), full, bd)
+    high = (s0 == MASK) & (conf[:, 0] > tau)
+    depth_of = {}
+    for n in range(len(parent)):
+        q = int(parent[n])
+        depth_of[n] = 0 if (q == -1 and n == 0 and high.any()) else (1 if q == -1 else depth_of[q] + 1)
+    widths = level_widths(W, D, full)
+    for level in range(2, D + 1):
+        kept = [n for n in depth_of if depth_of[n] == level]
+        parents = [n for n in depth_of if depth_of[n] == level - 1]
+        if not kept:
+            continue
+        assert len(kept) <= widths[level - 1]
+        assert all(score[a] >= score[b] for a, b in zip(kept, kept[1:]))
+        # every child the parents could generate, scored like the oracle
+        cands = []
+        for q in parents:
+            masked_low = [p for p in range(L) if tokens[q][p] == MASK and conf[p][0] <= tau]
+            p = min(masked_low, key=lambda x: (-float(conf[x][0]), x))
+            for j in range(bd):
+                cands.append(score[q] + math.log(float(conf[p][j])))
+        worst_kept = min(score[n] for n in kept)
+        assert sum(1 for c in cands if c > worst_kept) <= len(kept) - 1
