@@ -212,9 +212,12 @@ traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts
  * Phase 2, for levels l = 1 .. depth while Low has an l-th position q_l (Low ranked by
  *   C[p,0], larger first, smaller p on equal values):
  *   l = 1:  children j = 0 .. branch-1 of the root set q_1 to I[q_1, j]     (GenerateTopK);
- *   l > 1:  each kept node of level l-1 gets one child setting q_l to I[q_l, 0] (GenerateTop1);
+ *   l > 1:  each kept node of level l-1 gets branch_deep children setting q_l to I[q_l, j],
+ *           j = 0 .. branch_deep-1 (GenerateTop1 when branch_deep == 1, the hybrid policy;
+ *           2 = the "full top-2" policy of the expansion ablation);
  *   each level keeps its w_l best children by score (PruneByConfidence; generation order on
- *   equal scores), w_l = max(width - l + 1, 1) (hybrid, full == 0) or width (full == 1).
+ *   equal scores, scores compared in fp32), w_l = max(width - l + 1, 1) (hybrid, full == 0)
+ *   or width (full == 1).
  *   score = sum of log C over the candidates chosen on the path below the root (root: 0),
  *   accumulated in fp32 in path order.
  *   With H empty, node 0 is one threshold-decoding step of s0 (the top-1 fallback), so an
@@ -230,7 +233,7 @@ traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts
  *   the committed-state candidates of the next traj_accept call (its conf0 / idx0).
  * Each [k] candidate row must be non-increasing in confidence (as traj_confidence_topk
  * writes it): the first level's pruning keeps candidates 0 .. w_1-1 on that basis.
- * Limits: B >= 1; 1 <= L <= 64; 1 <= k <= 8; 1 <= branch <= k; width >= 1; depth >= 0;
+ * Limits: B >= 1; 1 <= L <= 64; 1 <= k <= 8; 1 <= branch, branch_deep <= k; width >= 1; depth >= 0;
  *   n_prev >= 0 (drafts per sequence in conf / idx; both may be NULL when n_prev == 0 or
  *   leaf == NULL); traj_tree_max_nodes(shape) <= n_max <= 64.
  *   A leaf[b] outside [-1, n_prev) is taken as -1 and sets TRAJ_DEV_BAD_LEAF.
@@ -241,10 +244,12 @@ typedef struct {
     int32_t width, depth, branch; /* W, D and the candidates tried at the first level  */
     int32_t full;                 /* 0 hybrid level widths, 1 full (width per level)   */
     int32_t n_max;                /* node slots per sequence in the outputs            */
+    int32_t branch_deep;          /* children per node below the first level, 1..k     */
 } traj_tree_shape;
 
 /* Largest node count the shape's tree can reach (1 + sum over levels l <= min(depth, L) of
- * c_l, c_1 = min(branch, w_1), c_l = min(w_l, c_{l-1})); -1 when the shape is invalid. */
+ * c_l, c_1 = min(branch, w_1), c_l = min(w_l, c_{l-1} * branch_deep)); -1 when the shape is
+ * invalid. */
 int32_t traj_tree_max_nodes(const traj_tree_shape* shape);
 
 traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const float* conf,

@@ -57,7 +57,7 @@ class Accepted(ctypes.Structure):
 class TreeShape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("L", ctypes.c_int32), ("k", ctypes.c_int32), ("n_prev", ctypes.c_int32),
                 ("width", ctypes.c_int32), ("depth", ctypes.c_int32), ("branch", ctypes.c_int32),
-                ("full", ctypes.c_int32), ("n_max", ctypes.c_int32)]
+                ("full", ctypes.c_int32), ("n_max", ctypes.c_int32), ("branch_deep", ctypes.c_int32)]
 
 
 _LIB = None
@@ -287,8 +287,8 @@ def accept(conf, idx, tokens, parent, committed, conf0, idx0, threshold, mode="e
 
 
 # ---------------------------------------------------------------- tree construction
-def tree_shape(B, L, k, width, depth, branch, full=False, n_prev=0, n_max=None):
-    sh = TreeShape(B, L, k, n_prev, width, depth, branch, 1 if full else 0, 0)
+def tree_shape(B, L, k, width, depth, branch, full=False, n_prev=0, n_max=None, branch_deep=1):
+    sh = TreeShape(B, L, k, n_prev, width, depth, branch, 1 if full else 0, 0, branch_deep)
     if n_max is None:
         n_max = int(_lib().traj_tree_max_nodes(ctypes.byref(sh)))
         if n_max < 0:
@@ -297,12 +297,13 @@ def tree_shape(B, L, k, width, depth, branch, full=False, n_prev=0, n_max=None):
     return sh
 
 
-def tree_max_nodes(B, L, k, width, depth, branch, full=False):
-    return int(_lib().traj_tree_max_nodes(ctypes.byref(tree_shape(B, L, k, width, depth, branch, full, n_max=0))))
+def tree_max_nodes(B, L, k, width, depth, branch, full=False, branch_deep=1):
+    return int(_lib().traj_tree_max_nodes(ctypes.byref(tree_shape(B, L, k, width, depth, branch, full, n_max=0,
+                                                                  branch_deep=branch_deep))))
 
 
 def build_tree(state, conf0, idx0, threshold, width, depth, branch, full=False, leaf=None, conf=None, idx=None,
-               n_max=None, out=None, stream=None):
+               n_max=None, out=None, stream=None, branch_deep=1):
     """Next step's draft tree (Alg. 1) from the accepted state; returns a dict of device
     tensors tokens [B,n_max,L], parent [B,n_max], n_nodes [B], score [B,n_max],
     conf_next / idx_next [B,L,k].  With ``leaf`` (traj_accept's leaf) the candidates come
@@ -319,7 +320,7 @@ def build_tree(state, conf0, idx0, threshold, width, depth, branch, full=False, 
         n_prev = conf.numel() // (B * L * k)
         if conf.numel() != B * n_prev * L * k or idx.numel() != conf.numel():
             raise ValueError("conf/idx must hold B*N*L*k entries")
-    sh = tree_shape(B, L, k, width, depth, branch, full, n_prev, n_max)
+    sh = tree_shape(B, L, k, width, depth, branch, full, n_prev, n_max, branch_deep)
     dev = state.device
     if out is None:
         out = {

@@ -230,15 +230,17 @@ traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int
 
 int32_t traj_tree_max_nodes(const traj_tree_shape* sh) {
     if (sh == nullptr || sh->B < 1 || sh->L < 1 || sh->L > kTreeMaxBlock || sh->k < 1 || sh->k > kTreeMaxK ||
-        sh->branch < 1 || sh->branch > sh->k || sh->width < 1 || sh->depth < 0 || sh->n_prev < 0 ||
-        (sh->full != 0 && sh->full != 1))
+        sh->branch < 1 || sh->branch > sh->k || sh->branch_deep < 1 || sh->branch_deep > sh->k || sh->width < 1 ||
+        sh->depth < 0 || sh->n_prev < 0 || (sh->full != 0 && sh->full != 1))
         return -1;
     int64_t total = 1, cnt = 0;
     const int levels = sh->depth < sh->L ? sh->depth : sh->L;
     for (int l = 1; l <= levels; ++l) {
         const int64_t w = sh->full ? sh->width : (sh->width - l + 1 > 1 ? sh->width - l + 1 : 1);
-        cnt = l == 1 ? (sh->branch < w ? sh->branch : w) : (w < cnt ? w : cnt);
+        const int64_t gen = l == 1 ? sh->branch : cnt * sh->branch_deep;
+        cnt = gen < w ? gen : w;
         total += cnt;
+        if (total > 0x7fffffff) return -1;
     }
     return (int32_t)total;
 }
@@ -253,11 +255,11 @@ traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const flo
     if (leaf != nullptr && shape->n_prev > 0 && (conf == nullptr || idx == nullptr)) return TRAJ_E_NULL;
     if ((conf_next == nullptr) != (idx_next == nullptr)) return TRAJ_E_NULL;
     if (shape->k < 1 || shape->k > kTreeMaxK || shape->branch < 1 || shape->branch > shape->k ||
-        (shape->full != 0 && shape->full != 1))
+        shape->branch_deep < 1 || shape->branch_deep > shape->k || (shape->full != 0 && shape->full != 1))
         return TRAJ_E_ARG;
     if (!(threshold == threshold)) return TRAJ_E_ARG;
     const int32_t need = traj_tree_max_nodes(shape);
-    if (need < 0 || shape->n_max < need || shape->n_max > kTreeMaxBlock) return TRAJ_E_SHAPE;
+    if (need < 0 || shape->n_max < need || shape->n_max > kTreeMaxNodes) return TRAJ_E_SHAPE;
     TreeParams p{};
     p.state = state;
     p.leaf = leaf;
@@ -278,6 +280,7 @@ traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const flo
     p.width = shape->width;
     p.depth = shape->depth;
     p.branch = shape->branch;
+    p.branch_deep = shape->branch_deep;
     p.full = shape->full;
     p.n_max = shape->n_max;
     p.tau = threshold;

@@ -1,14 +1,15 @@
 // Draft tree construction (Alg. 1): confidence stratification of the accepted block state,
-// top-k expansion at the first level, top-1 expansion deeper, each level pruned to its width
-// by path confidence.  One wave per sequence, lane = block position (L <= 64).
+// top-k expansion at the first level, deeper levels expanded with the top `branch_deep`
+// candidates (1 = the hybrid top-1 policy), each level pruned to its width by path confidence.
+// One wave per sequence, lane = block position (L <= 64).
 //
-// Every node of a level fills the same position: nodes differ only in the candidate chosen at
-// the first level's position, and all nodes of a level have the same masked set.  So the
-// positions visited are the low-confidence positions in rank order (q_1, q_2, ...), level 1
-// holds candidates 0 .. c_1-1 at q_1 (their scores fall with the candidate index, so pruning
-// keeps a prefix), and level l extends the first c_l nodes of level l-1 by the top-1 token at
-// q_l (equal increments keep the parents' order).  Node (l, i) is the root with q_1 set to
-// candidate i and q_2 .. q_l set to their top-1 tokens; its parent is node (l-1, i).
+// All nodes of a level share their masked set (every level fills one position, the same for
+// all of its nodes), so level l fills q_l, the l-th low-confidence position in rank order.
+// Level l's candidates are (kept node i of level l-1, candidate j of q_l) in generation order
+// (i major); each is ranked by score (sum of logf of the chosen confidences, fp32) with
+// generation order breaking ties, and the first w_l ranks become the level's nodes.  Node
+// states are built in LDS (a node's row = its parent's row plus one position) and written out
+// at the end.
 #pragma once
 
 #include "common.hpp"
@@ -17,7 +18,9 @@ namespace trajspec {
 
 constexpr int kTreeThreads = 64;
 constexpr int kTreeMaxBlock = 64;
+constexpr int kTreeMaxNodes = 64;
 constexpr int kTreeMaxK = 8;
+constexpr int kTreeMaxCand = kTreeMaxNodes * kTreeMaxK;  // candidates of one level
 
 struct TreeParams {
     const int32_t* state;  // [B,L]
@@ -32,7 +35,7 @@ struct TreeParams {
     float* score;          // [B,n_max] or null
     float* conf_next;      // [B,L,k] or null
     int32_t* idx_next;     // [B,L,k] or null
-    int B, L, k, n_prev, width, depth, branch, full, n_max;
+    int B, L, k, n_prev, width, depth, branch, branch_deep, full, n_max;
     float tau;
 };
 
@@ -42,7 +45,12 @@ __device__ __forceinline__ int tree_level_width(const TreeParams& P, int l) {
 }
 
 __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) {
-    __shared__ int pos[kTreeMaxBlock];  // low-confidence positions by rank
+    __shared__ int pos[kTreeMaxBlock];                 // low-confidence positions by rank
+    __shared__ int tok[kTreeMaxNodes][kTreeMaxBlock];  // node states
+    __shared__ int par[kTreeMaxNodes];
+    __shared__ float nsc[kTreeMaxNodes];               // node scores
+    __shared__ float csc[kTreeMaxCand];                // candidate scores of the current level
+    __shared__ int cnode[kTreeMaxCand];                // candidate -> new node slot, -1 if pruned
     const int b = blockIdx.x;
     const int p = threadIdx.x;
     const int L = P.L, k = P.k;
@@ -58,7 +66,6 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
 
     const int s = in ? P.state[(int64_t)b * L + p] : 0;
     const float c0 = in ? C[p * k] : 0.f;
-    const int top1 = in ? I[p * k] : 0;
     const bool masked = in && s == -1;
     const bool hi = masked && c0 > P.tau;
     const bool low = masked && !hi;
@@ -71,8 +78,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
         }
     }
 
-    // rank of this low position: low positions of larger confidence, or equal confidence
-    // and smaller index, come first
+    // rank of this low position: larger confidence first, then smaller index
     int rank = 0;
     for (int q = 0; q < L; ++q) {
         const float cq = __shfl(c0, q);
@@ -80,61 +86,72 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
         rank += (lq && (cq > c0 || (cq == c0 && q < p))) ? 1 : 0;
     }
     if (low) pos[rank] = p;
-    __syncthreads();
     const int nlow = __popcll(lmask);
-
-    const int root_tok = hi ? top1 : s;
-    int32_t* tok_b = P.tokens + (int64_t)b * P.n_max * L;
-    int32_t* par_b = P.parent + (int64_t)b * P.n_max;
-    float* sc_b = P.score != nullptr ? P.score + (int64_t)b * P.n_max : nullptr;
+    const int root_tok = hi ? (in ? I[p * k] : 0) : s;
 
     int n = 0;
     const bool has_root = hmask != 0ull;
     if (has_root) {
-        if (in) tok_b[p] = root_tok;
+        if (in) tok[0][p] = root_tok;
         if (p == 0) {
-            par_b[0] = -1;
-            if (sc_b != nullptr) sc_b[0] = 0.f;
+            par[0] = -1;
+            nsc[0] = 0.f;
         }
         n = 1;
     }
-    const int base = has_root ? 0 : -1;
-    float sc[kTreeMaxK];  // scores of the previous level's nodes (uniform)
-    int prev_first = 0, cnt = 0;
-    const int q1 = nlow > 0 ? pos[0] : -1;
+    __syncthreads();
+    int prev_first = 0, prev_cnt = 1;  // level 0: the root (node 0, or the state itself)
     for (int l = 1; l <= P.depth && l <= nlow; ++l) {
-        const int ql = pos[l - 1];
+        const int q = pos[l - 1];
+        const int bl = l == 1 ? P.branch : P.branch_deep;
+        const int M = prev_cnt * bl;
         const int w = tree_level_width(P, l);
-        const int c = l == 1 ? min(P.branch, w) : min(w, cnt);
-        const float inc = l == 1 ? 0.f : logf(C[ql * k]);
-#pragma unroll
-        for (int i = 0; i < kTreeMaxK; ++i) {
-            if (i >= c) break;
-            const int node = n + i;
-            int t = root_tok;
-            if (p == q1) {
-                t = I[p * k + i];
-            } else if (low && rank >= 1 && rank < l) {
-                t = top1;
+        for (int m = p; m < M; m += kTreeThreads) {
+            const int i = m / bl, j = m - i * bl;
+            const float base = (l == 1) ? 0.f : nsc[prev_first + i];
+            csc[m] = base + logf(C[q * k + j]);
+        }
+        __syncthreads();
+        for (int m = p; m < M; m += kTreeThreads) {
+            const float sm = csc[m];
+            int r = 0;
+            for (int m2 = 0; m2 < M; ++m2) {
+                const float s2 = csc[m2];
+                r += (s2 > sm || (s2 == sm && m2 < m)) ? 1 : 0;
             }
-            if (in) tok_b[(int64_t)node * L + p] = t;
-            const float s_node = l == 1 ? logf(C[q1 * k + i]) : sc[i] + inc;
-            sc[i] = s_node;
-            if (p == 0) {
-                par_b[node] = l == 1 ? base : prev_first + i;
-                if (sc_b != nullptr) sc_b[node] = s_node;
+            const int slot = r < w ? n + r : -1;
+            cnode[m] = slot;
+            if (slot >= 0) {
+                const int i = m / bl;
+                par[slot] = (l == 1) ? (has_root ? 0 : -1) : prev_first + i;
+                nsc[slot] = sm;
             }
         }
+        __syncthreads();
+        // node states: the parent's row with q set to the chosen candidate
+        for (int m = 0; m < M; ++m) {
+            const int slot = cnode[m];
+            if (slot < 0) continue;
+            const int i = m / bl, j = m - i * bl;
+            const int src = (l == 1) ? -1 : prev_first + i;
+            int t = src < 0 ? root_tok : tok[src][in ? p : 0];
+            if (p == q) t = I[q * k + j];
+            if (in) tok[slot][p] = t;
+        }
+        __syncthreads();
+        const int c = min(w, M);
         prev_first = n;
+        prev_cnt = c;
         n += c;
-        cnt = c;
     }
-    for (int node = n; node < P.n_max; ++node) {
-        if (in) tok_b[(int64_t)node * L + p] = s;
-        if (p == 0) {
-            par_b[node] = -1;
-            if (sc_b != nullptr) sc_b[node] = -__builtin_huge_valf();
-        }
+
+    int32_t* tok_b = P.tokens + (int64_t)b * P.n_max * L;
+    for (int node = 0; node < P.n_max; ++node) {
+        if (in) tok_b[(int64_t)node * L + p] = node < n ? tok[node][p] : s;
+    }
+    for (int node = p; node < P.n_max; node += kTreeThreads) {
+        P.parent[(int64_t)b * P.n_max + node] = node < n ? par[node] : -1;
+        if (P.score != nullptr) P.score[(int64_t)b * P.n_max + node] = node < n ? nsc[node] : -__builtin_huge_valf();
     }
     if (p == 0) P.n_nodes[b] = n;
 }

@@ -137,7 +137,7 @@ def test_tree_argument_errors_and_max_nodes():
     lib = _lib.load()
 
     def shape(**kw):
-        d = dict(B=2, L=8, k=3, n_prev=0, width=3, depth=3, branch=3, full=0, n_max=7)
+        d = dict(B=2, L=8, k=3, n_prev=0, width=3, depth=3, branch=3, full=0, n_max=7, branch_deep=1)
         d.update(kw)
         return _lib.TreeShape(**d)
 
@@ -150,16 +150,18 @@ def test_tree_argument_errors_and_max_nodes():
     assert call(shape(n_prev=4), leaf=FAKE) == 1                 # leaf given, conf/idx missing
     assert call(shape(), nxt=(FAKE, None)) == 1                  # conf_next without idx_next
     assert call(shape(k=9)) == 7 and call(shape(branch=4)) == 7 and call(shape(full=2)) == 7
+    assert call(shape(branch_deep=0)) == 7 and call(shape(branch_deep=4)) == 7
     assert call(shape(), tau=float("nan")) == 7
     assert call(shape(L=65)) == 2 and call(shape(n_max=6)) == 2 and call(shape(n_max=65)) == 2
     assert call(shape(width=0)) == 2 and call(shape(depth=-1)) == 2
-    for W, D, br, full, L in [(3, 3, 3, 0, 8), (3, 3, 3, 1, 8), (2, 5, 3, 0, 8), (4, 2, 2, 0, 8), (1, 1, 1, 0, 8),
-                              (3, 0, 3, 0, 8), (3, 6, 2, 1, 4), (8, 8, 8, 1, 64)]:
+    for W, D, br, full, L, bd in [(3, 3, 3, 0, 8, 1), (3, 3, 3, 1, 8, 1), (2, 5, 3, 0, 8, 1), (4, 2, 2, 0, 8, 1),
+                                  (1, 1, 1, 0, 8, 1), (3, 0, 3, 0, 8, 1), (3, 6, 2, 1, 4, 1), (8, 8, 8, 1, 64, 1),
+                                  (2, 2, 2, 1, 8, 2), (4, 3, 2, 1, 8, 2), (6, 4, 1, 0, 16, 3)]:
         cnt, total = 0, 1
         for level, w in enumerate(level_widths(W, min(D, L), bool(full)), start=1):
-            cnt = min(br, w) if level == 1 else min(w, cnt)
+            cnt = min(br, w) if level == 1 else min(w, cnt * bd)
             total += cnt
-        sh = shape(width=W, depth=D, branch=br, full=full, L=L, k=8)
+        sh = shape(width=W, depth=D, branch=br, full=full, L=L, k=8, branch_deep=bd)
         assert lib.traj_tree_max_nodes(ctypes.byref(sh)) == total
 
 
