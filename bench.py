@@ -301,6 +301,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seqs", type=int, default=1)
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the measurements beside the step (warm cache, tree build, inter-block), e.g. "
+                         "for a kernel trace of the step alone")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run three 1 GiB device-to-device copies (for scaling rocprofv3 FETCH_SIZE / "
                          "WRITE_SIZE readings) and exit")
@@ -361,13 +364,13 @@ def main():
     flops = attn_flops(wl, x.d["parent"])
     a_tflops = flops / (t_attn * 1e-3) / 1e12
     l_gbs = logit_bytes(wl) / (t_conf * 1e-3) / 1e9
-    warm = time_warm(x, buf, tau, stream, args.steps) if n_copies > 1 else None
+    warm = time_warm(x, buf, tau, stream, args.steps) if n_copies > 1 and not args.no_extras else None
     # the last timed step used copies[(K-1) % n]; rerun copy 0 so outputs match x
     run_step(x, buf, tau, stream)
     torch.cuda.synchronize()
     acc_main = buf.acc["n_accepted"].cpu().numpy()
-    tree = time_tree_build(x, buf, tau, stream)
-    inter = time_interblock(x, buf, tau, stream)
+    tree = None if args.no_extras else time_tree_build(x, buf, tau, stream)
+    inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
     result = {
@@ -408,7 +411,8 @@ def main():
         "attention_hbm_bytes_per_launch": attn_bytes(wl),
         "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
         "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},
-        "warm": warm if warm is not None else "inputs exceed the 256 MB Infinity Cache: every step reads HBM",
+        "warm": warm if warm is not None or args.no_extras else
+                "inputs exceed the 256 MB Infinity Cache: every step reads HBM",
         "tree_build": tree,
         "interblock": inter,
         "device_status": status,

@@ -51,6 +51,8 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
     __shared__ float nsc[kTreeMaxNodes];               // node scores
     __shared__ float csc[kTreeMaxCand];                // candidate scores of the current level
     __shared__ int cnode[kTreeMaxCand];                // candidate -> new node slot, -1 if pruned
+    __shared__ float cs[kTreeMaxBlock][kTreeMaxK];     // the state's candidates, staged once
+    __shared__ int is[kTreeMaxBlock][kTreeMaxK];
     const int b = blockIdx.x;
     const int p = threadIdx.x;
     const int L = P.L, k = P.k;
@@ -71,10 +73,16 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
     const bool low = masked && !hi;
     const uint64_t hmask = ballot64(hi);
     const uint64_t lmask = ballot64(low);
-    if (in && P.conf_next != nullptr) {
+    if (in) {
         for (int j = 0; j < k; ++j) {
-            P.conf_next[((int64_t)b * L + p) * k + j] = C[p * k + j];
-            P.idx_next[((int64_t)b * L + p) * k + j] = I[p * k + j];
+            cs[p][j] = C[p * k + j];
+            is[p][j] = I[p * k + j];
+        }
+        if (P.conf_next != nullptr) {
+            for (int j = 0; j < k; ++j) {
+                P.conf_next[((int64_t)b * L + p) * k + j] = cs[p][j];
+                P.idx_next[((int64_t)b * L + p) * k + j] = is[p][j];
+            }
         }
     }
 
@@ -87,7 +95,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
     }
     if (low) pos[rank] = p;
     const int nlow = __popcll(lmask);
-    const int root_tok = hi ? (in ? I[p * k] : 0) : s;
+    const int root_tok = hi ? is[p][0] : s;
 
     int n = 0;
     const bool has_root = hmask != 0ull;
@@ -109,7 +117,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
         for (int m = p; m < M; m += kTreeThreads) {
             const int i = m / bl, j = m - i * bl;
             const float base = (l == 1) ? 0.f : nsc[prev_first + i];
-            csc[m] = base + logf(C[q * k + j]);
+            csc[m] = base + logf(cs[q][j]);
         }
         __syncthreads();
         for (int m = p; m < M; m += kTreeThreads) {
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeParams P) 
             const int i = m / bl, j = m - i * bl;
             const int src = (l == 1) ? -1 : prev_first + i;
             int t = src < 0 ? root_tok : tok[src][in ? p : 0];
-            if (p == q) t = I[q * k + j];
+            if (p == q) t = is[q][j];
             if (in) tok[slot][p] = t;
         }
         __syncthreads();
