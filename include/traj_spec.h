@@ -19,6 +19,8 @@
  *   5. traj_interblock_trigger and traj_verify_attn_peers -- inter-block speculation
  *                               (Sec. 3.4): the trigger, and attention for the joint trees of
  *                               two blocks with root-to-root visibility.
+ *   6. traj_verify_layer     -- a whole decoder layer of the verification forward pass around
+ *                               call 1 (norms, projections, RoPE, MLP; synthetic weights).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
@@ -275,6 +277,49 @@ traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const flo
 traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int32_t B, int32_t L,
                                     int32_t k, float threshold, uint8_t* trigger, float* c_cur,
                                     float* c_next, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * 6. Verification layer  (Sec. 3.2 "Complexity analysis": the drafts go through one
+ *    concatenated forward pass; Sec. 3.3: with the trajectory mask; App. A: dual cache)
+ *
+ * One pre-norm decoder layer of the 8B-shaped diffusion LMs over the packed draft tokens,
+ * updating their residual stream x in place:
+ *   xn = RMSNorm(x) * attn_norm;   [q | k | v] = xn @ w_qkv;   RoPE on q and k;
+ *   x += traj_verify_attn(q, k_cache, v_cache, k, v, draft_parent) @ w_o;
+ *   xn = RMSNorm(x) * mlp_norm;    [g | u] = xn @ w_gate_up;   x += (silu(g) * u) @ w_down.
+ * RMSNorm: x / sqrt(mean(x^2) + rms_eps).  RoPE: pairs (d, d + D/2) of each q / k head rotate
+ * by pos * rope_theta^(-2d/D), pos = pos0[b] + p for block position p of every draft (the drafts
+ * are alternative states of the same block); the cache K is expected with RoPE applied.
+ * Every intermediate is rounded to bf16 (the activations' storage type), arithmetic is fp32;
+ * the projections are library GEMMs (hipBLASLt, fp32 accumulation).
+ * Layouts (bf16, row-major): x [B,N,L,hidden]; attn_norm, mlp_norm [hidden];
+ *   w_qkv [hidden, (Hq + 2 Hkv) D]; w_o [Hq D, hidden]; w_gate_up [hidden, 2 inter] (gate then
+ *   up); w_down [inter, hidden]; k_cache / v_cache and draft_parent as traj_verify_attn;
+ *   pos0 [B] int32 (NULL = 0).  shape is the attention shape of the call (scale included).
+ * workspace: at least traj_verify_layer_workspace_size() bytes, 256-byte aligned (all
+ * intermediates plus the GEMMs' scratch).
+ * Limits: those of traj_verify_attn; hidden == Hq * D; hidden % 8 == 0; inter % 8 == 0.
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    int32_t hidden, inter;
+    float rms_eps, rope_theta;
+} traj_layer_dims;
+
+typedef struct {
+    const void* attn_norm;
+    const void* w_qkv;
+    const void* w_o;
+    const void* mlp_norm;
+    const void* w_gate_up;
+    const void* w_down;
+} traj_layer_weights;
+
+size_t traj_verify_layer_workspace_size(const traj_attn_shape* shape, const traj_layer_dims* dims);
+
+traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const traj_layer_dims* dims,
+                              const void* k_cache, const void* v_cache, const int32_t* draft_parent,
+                              const int32_t* pos0, const traj_attn_shape* shape, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Utilities

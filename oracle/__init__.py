@@ -17,6 +17,8 @@ Decoding for Diffusion LLMs):
   by path confidence.
 * :mod:`oracle.interblock` -- inter-block speculation trigger and the joint
   tree's root-to-root visibility (Sec. 3.4, App. D).
+* :mod:`oracle.layer`      -- one verification decoder layer around the attention
+  (RMSNorm, projections, rotary positions, SwiGLU MLP) with bf16 storage.
 * :mod:`oracle.brute`      -- scalar-loop re-derivations used only to pin the
   functions above on tiny inputs.
 
@@ -43,6 +45,7 @@ from .accept import (  # noqa: E402
     fragile_states,
 )
 from .tree import build_tree, build_tree_batch, gather_state_scores, level_widths  # noqa: E402
+from .layer import bf16_round, verify_layer  # noqa: E402
 from .interblock import block_top1_confidence, interblock_trigger, interblock_trigger_batch, joint_peers  # noqa: E402
 
 __all__ = [
@@ -65,4 +68,6 @@ __all__ = [
     "interblock_trigger",
     "interblock_trigger_batch",
     "joint_peers",
+    "bf16_round",
+    "verify_layer",
 ]

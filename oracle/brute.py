@@ -114,3 +114,63 @@ def accept_by_paths(tokens, parent, committed, conf0, idx0, conf, idx, tau, mode
             best = g
             longest_leaf = end
     return greedy_leaf, longest_leaf
+
+
+def _bf16(x):
+    """Nearest-even bf16 of a float, through fp32 (struct-level bit manipulation)."""
+    import struct
+    b = struct.unpack("<I", struct.pack("<f", float(x)))[0]
+    b = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16) << 16
+    return struct.unpack("<f", struct.pack("<I", b & 0xFFFFFFFF))[0]
+
+
+def layer_scalar(x, weights, k_cache, v_cache, parent, Hq, pos0, rms_eps, rope_theta):
+    """Nested-loop verification layer (one token, one feature at a time) with the same bf16
+    rounding points as :func:`oracle.layer.verify_layer`."""
+    B, N, L, hidden = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
+    D = hidden // Hq
+    Hkv = len(k_cache[0][0]) if len(k_cache[0]) else Hq
+    inter = len(weights["w_down"])
+    W = weights
+    out = [[[list(map(float, x[b][n][p])) for p in range(L)] for n in range(N)] for b in range(B)]
+
+    def norm(v, g):
+        ms = math.fsum(t * t for t in v) / len(v)
+        inv = 1.0 / math.sqrt(ms + rms_eps)
+        return [_bf16(v[i] * inv * float(g[i])) for i in range(len(v))]
+
+    def matvec(v, m, cols):
+        return [math.fsum(v[i] * float(m[i][j]) for i in range(len(v))) for j in range(cols)]
+
+    qs = [[[None] * L for _ in range(N)] for _ in range(B)]
+    ks = [[[None] * L for _ in range(N)] for _ in range(B)]
+    vs = [[[None] * L for _ in range(N)] for _ in range(B)]
+    for b in range(B):
+        for n in range(N):
+            for p in range(L):
+                xn = norm(out[b][n][p], W["attn_norm"])
+                qkv = [_bf16(t) for t in matvec(xn, W["w_qkv"], (Hq + 2 * Hkv) * D)]
+                pos = (0 if pos0 is None else int(pos0[b])) + p
+                heads = []
+                for hh in range(Hq + Hkv):
+                    seg = qkv[hh * D:(hh + 1) * D]
+                    rot = [0.0] * D
+                    for d in range(D // 2):
+                        a = pos * rope_theta ** (-2.0 * d / D)
+                        rot[d] = _bf16(seg[d] * math.cos(a) - seg[d + D // 2] * math.sin(a))
+                        rot[d + D // 2] = _bf16(seg[d + D // 2] * math.cos(a) + seg[d] * math.sin(a))
+                    heads.append(rot)
+                qs[b][n][p] = heads[:Hq]
+                ks[b][n][p] = heads[Hq:]
+                vs[b][n][p] = [qkv[(Hq + Hkv + hh) * D:(Hq + Hkv + hh + 1) * D] for hh in range(Hkv)]
+    att = attention_scalar(qs, k_cache, v_cache, ks, vs, parent)
+    for b in range(B):
+        for n in range(N):
+            for p in range(L):
+                a = [_bf16(t) for hh in range(Hq) for t in att[b][n][p][hh]]
+                h = [_bf16(out[b][n][p][i] + t) for i, t in enumerate(matvec(a, W["w_o"], hidden))]
+                xn = norm(h, W["mlp_norm"])
+                gu = [_bf16(t) for t in matvec(xn, W["w_gate_up"], 2 * inter)]
+                act = [_bf16(gu[i] / (1.0 + math.exp(-gu[i])) * gu[inter + i]) for i in range(inter)]
+                out[b][n][p] = [_bf16(h[i] + t) for i, t in enumerate(matvec(act, W["w_down"], hidden))]
+    return out

@@ -1,0 +1,87 @@
+"""Oracle: one verification decoder layer around the trajectory-masked attention.
+
+TEST INFRASTRUCTURE ONLY -- see the package docstring.
+
+The verification step runs every draft block through the model in one concatenated forward
+pass (Sec. 3.2 "Complexity analysis"; App. A: only block K/V is recomputed, the dual cache
+supplies the rest).  One pre-norm decoder layer of the 8B-shaped diffusion LMs the paper runs
+(LLaMA-style blocks: RMSNorm, rotary positions, SwiGLU MLP), over the packed draft tokens:
+
+    xn = rmsnorm(x) * attn_norm;     [q | k | v] = xn @ w_qkv;     q, k rotated;
+    x  = x + attention(q, k_cache, v_cache, k, v, parent) @ w_o;
+    xn = rmsnorm(x) * mlp_norm;      [g | u] = xn @ w_gate_up;
+    x  = x + (silu(g) * u) @ w_down
+
+* rmsnorm(x) = x / sqrt(mean(x^2) + eps) per token.
+* Rotary positions: pairs (d, d + D/2) of each q / k head rotate by pos * theta^(-2d/D); token
+  p of every draft of a block sits at position pos0[b] + p (the drafts are alternative states
+  of the same block, Sec. 3.2 "Tree construction").
+* Arithmetic in fp64; values are rounded to bf16 (round to nearest even, through fp32) wherever
+  the library stores an activation, so that both sides see the same stored intermediates.
+"""
+
+import numpy as np
+
+from .attention import verify_attention
+
+
+def bf16_round(a):
+    """Round to bf16 (nearest even) through fp32; returns float64."""
+    a32 = np.asarray(a, dtype=np.float64).astype(np.float32)
+    bits = a32.view(np.uint32).astype(np.uint64)
+    rounded = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
+    return rounded.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def rmsnorm(x, w, eps):
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * np.asarray(w, dtype=np.float64)
+
+
+def rope(x, pos, theta):
+    """x [T, H, D], pos [T]: rotate pairs (d, d + D/2) by pos * theta^(-2d/D)."""
+    x = np.asarray(x, dtype=np.float64)
+    D = x.shape[-1]
+    half = D // 2
+    inv_freq = theta ** (-2.0 * np.arange(half) / D)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]  # [T, half]
+    c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def silu(g):
+    return g / (1.0 + np.exp(-g))
+
+
+def verify_layer(x, weights, k_cache, v_cache, parent, Hq, pos0=None, rms_eps=1e-5, rope_theta=500000.0,
+                 scale=None):
+    """x [B,N,L,hidden] (bf16 values); weights: attn_norm [hidden], w_qkv [hidden, (Hq+2Hkv)D],
+    w_o [Hq D, hidden], mlp_norm [hidden], w_gate_up [hidden, 2I], w_down [I, hidden].
+    Returns the updated x (float64 holding bf16 values)."""
+    r = bf16_round
+    x = np.asarray(x, dtype=np.float64)
+    B, N, L, hidden = x.shape
+    D = hidden // Hq
+    Hkv = k_cache.shape[2]
+    T = B * N * L
+    W = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
+    inter = W["w_down"].shape[0]
+    pos = np.array([(0 if pos0 is None else int(pos0[b])) + p for b in range(B) for _ in range(N) for p in range(L)])
+
+    h = x.reshape(T, hidden)
+    xn = r(rmsnorm(h, W["attn_norm"], rms_eps))
+    qkv = r(xn @ W["w_qkv"])
+    q = qkv[:, :Hq * D].reshape(T, Hq, D)
+    k = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
+    v = qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D)
+    q, k = r(rope(q, pos, rope_theta)), r(rope(k, pos, rope_theta))
+    a = verify_attention(q.reshape(B, N, L, Hq, D), k_cache, v_cache, k.reshape(B, N, L, Hkv, D),
+                         v.reshape(B, N, L, Hkv, D), parent, scale=scale)
+    a = r(a).reshape(T, Hq * D)
+    h = r(h + a @ W["w_o"])
+    xn = r(rmsnorm(h, W["mlp_norm"], rms_eps))
+    gu = r(xn @ W["w_gate_up"])
+    act = r(silu(gu[:, :inter]) * gu[:, inter:])
+    h = r(h + act @ W["w_down"])
+    return h.reshape(B, N, L, hidden)

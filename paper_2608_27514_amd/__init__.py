@@ -20,6 +20,9 @@ and inter-block speculation (Sec. 3.4):
 * :func:`interblock_trigger` -- whether the next block is confident enough to
   speculate on both blocks; :func:`verify_attn` with ``peers`` (see
   :func:`joint_peers`) verifies the joint trees with root-to-root visibility.
+
+and :func:`verify_layer`, a whole decoder layer of the verification forward pass around the
+attention (norms, projections on hipBLASLt, RoPE, SwiGLU MLP).
 """
 
 from ._lib import (  # noqa: F401
@@ -34,6 +37,8 @@ from ._lib import (  # noqa: F401
     device_status,
     interblock_trigger,
     joint_peers,
+    layer_workspace_size,
+    verify_layer,
     load,
     tree_max_nodes,
     verify_attn,

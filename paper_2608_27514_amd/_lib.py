@@ -60,6 +60,15 @@ class TreeShape(ctypes.Structure):
                 ("full", ctypes.c_int32), ("n_max", ctypes.c_int32), ("branch_deep", ctypes.c_int32)]
 
 
+class LayerDims(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_theta", ctypes.c_float)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
 _LIB = None
 
 EXPORTS = {
@@ -78,6 +87,11 @@ EXPORTS = {
                                                  ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_void_p, ctypes.c_void_p]),
     "traj_tree_max_nodes": (ctypes.c_int32, [ctypes.POINTER(TreeShape)]),
+    "traj_verify_layer_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(AttnShape), ctypes.POINTER(LayerDims)]),
+    "traj_verify_layer": (ctypes.c_int32, [ctypes.c_void_p, ctypes.POINTER(LayerWeights), ctypes.POINTER(LayerDims),
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.POINTER(AttnShape), ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_void_p]),
     "traj_build_tree": (ctypes.c_int32, [ctypes.c_void_p] * 6 + [ctypes.POINTER(TreeShape), ctypes.c_float]
                         + [ctypes.c_void_p] * 7),
     "traj_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
@@ -337,6 +351,44 @@ def build_tree(state, conf0, idx0, threshold, width, depth, branch, full=False, 
                                 _ptr(out.get("idx_next")), _stream(stream))
     _check(st, "traj_build_tree")
     return out
+
+
+# ---------------------------------------------------------------- verification layer
+LAYER_WEIGHTS = ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+
+
+def layer_workspace_size(B, N, L, Hq, Hkv, D, S, hidden, inter, rms_eps=1e-5, rope_theta=500000.0):
+    sh = AttnShape(B, N, L, Hq, Hkv, D, S, 0.0)
+    return int(_lib().traj_verify_layer_workspace_size(ctypes.byref(sh),
+                                                       ctypes.byref(LayerDims(hidden, inter, rms_eps, rope_theta))))
+
+
+def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inter=None, rms_eps=1e-5,
+                 rope_theta=500000.0, scale=0.0, workspace=None, stream=None):
+    """One verification decoder layer over the packed draft tokens; updates x [B,N,L,hidden]
+    (bf16) in place and returns it.  ``weights`` maps LAYER_WEIGHTS names to bf16 tensors."""
+    B, N, L, hidden = x.shape
+    D = hidden // Hq
+    S, Hkv = k_cache.shape[1], k_cache.shape[2]
+    if inter is None:
+        inter = weights["w_down"].shape[0]
+    _dev(x, "x", torch.bfloat16)
+    for n in LAYER_WEIGHTS:
+        _dev(weights[n], n, torch.bfloat16)
+    _dev(draft_parent, "draft_parent", torch.int32)
+    if pos0 is not None:
+        _dev(pos0, "pos0", torch.int32)
+    sh = AttnShape(B, N, L, Hq, Hkv, D, S, float(scale))
+    dims = LayerDims(hidden, inter, rms_eps, rope_theta)
+    need = int(_lib().traj_verify_layer_workspace_size(ctypes.byref(sh), ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    lw = LayerWeights(*[weights[n].data_ptr() for n in LAYER_WEIGHTS])
+    st = _lib().traj_verify_layer(_ptr(x), ctypes.byref(lw), ctypes.byref(dims), _ptr(k_cache), _ptr(v_cache),
+                                  _ptr(draft_parent), _ptr(pos0), ctypes.byref(sh), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "traj_verify_layer")
+    return x
 
 
 def device_status(reset=True, stream=None):

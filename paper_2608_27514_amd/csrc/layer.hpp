@@ -1,0 +1,118 @@
+// One verification layer around the trajectory-masked attention (a pre-norm decoder layer of
+// the 8B-shaped diffusion LMs the method runs on): the elementwise kernels between the
+// library GEMMs.  All activations are bf16 in HBM, arithmetic in fp32.
+//   rmsnorm_kernel     out = x / sqrt(mean(x^2) + eps) * w            (one workgroup per token)
+//   rope_split_kernel  [q | k | v] rows of the QKV projection -> q, k_draft, v_draft in the
+//                      attention's layouts, rotary position embedding on q and k (pairs d and
+//                      d + D/2, angle = pos * theta^(-2d/D)); token p of every draft of a block
+//                      sits at position pos0[b] + p (the drafts are alternative states of the
+//                      same block)
+//   swiglu_kernel      act = silu(gate) * up from the [gate | up] rows of the gate/up projection
+#pragma once
+
+#include "common.hpp"
+
+namespace trajspec {
+
+constexpr int kLayerThreads = 256;
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+    return __builtin_bit_cast(uint16_t, (__bf16)f);  // round to nearest even
+}
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float t = 0.f;
+    for (int w = 0; w < kLayerThreads / 64; ++w) t += red[w];
+    __syncthreads();
+    return t;
+}
+
+// x, out: [T, hidden] bf16 (rows contiguous); w: [hidden].  hidden % 8 == 0.
+__global__ __launch_bounds__(kLayerThreads) void rmsnorm_kernel(const uint16_t* __restrict__ x,
+                                                                const uint16_t* __restrict__ w,
+                                                                uint16_t* __restrict__ out, int hidden, float eps) {
+    __shared__ float red[kLayerThreads / 64];
+    const uint16_t* xr = x + (int64_t)blockIdx.x * hidden;
+    uint16_t* orow = out + (int64_t)blockIdx.x * hidden;
+    const int nv = hidden / 8;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < nv; i += kLayerThreads) {
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(xr + 8 * i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float a = bf16_lo(v[e]), b = bf16_hi(v[e]);
+            ss += a * a + b * b;
+        }
+    }
+    const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)hidden + eps);
+    for (int i = threadIdx.x; i < nv; i += kLayerThreads) {
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(xr + 8 * i);
+        const u32x4_t g = *reinterpret_cast<const u32x4_t*>(w + 8 * i);
+        u32x4_t o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float a = bf16_lo(v[e]) * inv * bf16_lo(g[e]);
+            const float b = bf16_hi(v[e]) * inv * bf16_hi(g[e]);
+            o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+        }
+        *reinterpret_cast<u32x4_t*>(orow + 8 * i) = o;
+    }
+}
+
+// qkv: [T, (Hq + 2 Hkv) D] rows [q heads | k heads | v heads]; token t = (b N + n) L + p.
+// q: [T, Hq, D], kd / vd: [T, Hkv, D].  One workgroup per token.
+__global__ __launch_bounds__(kLayerThreads) void rope_split_kernel(const uint16_t* __restrict__ qkv,
+                                                                   const int32_t* __restrict__ pos0,
+                                                                   uint16_t* __restrict__ q, uint16_t* __restrict__ kd,
+                                                                   uint16_t* __restrict__ vd, int NL, int L, int Hq,
+                                                                   int Hkv, int D, float log2_theta) {
+    const int t = blockIdx.x;
+    const int b = t / NL;
+    const int p = t % L;
+    const float pos = (float)(pos0 != nullptr ? pos0[b] + p : p);
+    const int width = (Hq + 2 * Hkv) * D;
+    const uint16_t* row = qkv + (int64_t)t * width;
+    const int half = D / 2;
+    // rotated pairs of the q and k heads
+    for (int i = threadIdx.x; i < (Hq + Hkv) * half; i += kLayerThreads) {
+        const int head = i / half, d = i - head * half;
+        const float inv_freq = exp2f(-(2.0f * d / (float)D) * log2_theta);
+        float sn, cs;
+        sincosf(pos * inv_freq, &sn, &cs);
+        const uint16_t* src = row + head * D;
+        const float x1 = bf16_bits_to_float(src[d]), x2 = bf16_bits_to_float(src[d + half]);
+        uint16_t* dst = head < Hq ? q + ((int64_t)t * Hq + head) * D : kd + ((int64_t)t * Hkv + (head - Hq)) * D;
+        dst[d] = f2bf(x1 * cs - x2 * sn);
+        dst[d + half] = f2bf(x2 * cs + x1 * sn);
+    }
+    // v heads: copied
+    const uint16_t* vsrc = row + (Hq + Hkv) * D;
+    uint16_t* vdst = vd + (int64_t)t * Hkv * D;
+    for (int i = threadIdx.x; i < Hkv * D; i += kLayerThreads) vdst[i] = vsrc[i];
+}
+
+// gu: [T, 2 I] rows [gate | up]; act: [T, I].  grid (ceil(I / (8 * threads)), T); I % 8 == 0.
+__global__ __launch_bounds__(kLayerThreads) void swiglu_kernel(const uint16_t* __restrict__ gu,
+                                                               uint16_t* __restrict__ act, int I) {
+    const int t = blockIdx.y;
+    const int i = blockIdx.x * kLayerThreads + threadIdx.x;  // 8-element chunk
+    if (i >= I / 8) return;
+    const u32x4_t g = *reinterpret_cast<const u32x4_t*>(gu + (int64_t)t * 2 * I + 8 * i);
+    const u32x4_t u = *reinterpret_cast<const u32x4_t*>(gu + (int64_t)t * 2 * I + I + 8 * i);
+    u32x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float g0 = bf16_lo(g[e]), g1 = bf16_hi(g[e]);
+        const float a = g0 / (1.0f + __expf(-g0)) * bf16_lo(u[e]);
+        const float c = g1 / (1.0f + __expf(-g1)) * bf16_hi(u[e]);
+        o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(c) << 16);
+    }
+    *reinterpret_cast<u32x4_t*>(act + (int64_t)t * I + 8 * i) = o;
+}
+
+}  // namespace trajspec

@@ -2,7 +2,12 @@
 // One translation unit: the kernels live in the headers included below.
 #include <hip/hip_runtime.h>
 
+#include <hipblaslt/hipblaslt.h>
+
 #include <cmath>
+#include <map>
+#include <mutex>
+#include <tuple>
 #include <cstdint>
 
 #include "../../include/traj_spec.h"
@@ -10,6 +15,7 @@
 #include "common.hpp"
 #include "conf_topk.hpp"
 #include "interblock.hpp"
+#include "layer.hpp"
 #include "tree.hpp"
 #include "verify_attn.hpp"
 
@@ -94,6 +100,107 @@ traj_status launch_topk(const void* logits, const traj_logits_shape* sh, int k, 
         case 4: return launch_topk_k<T, 4>(logits, sh, k, conf, idx, ws, ws_bytes, st);
         default: return launch_topk_k<T, 8>(logits, sh, k, conf, idx, ws, ws_bytes, st);
     }
+}
+
+// ------------------------------------------------------------------ verification layer
+constexpr size_t kLtWorkspace = 32u << 20;  // hipBLASLt scratch inside the layer workspace
+
+struct LtDevice {
+    hipblasLtHandle_t handle = nullptr;
+    std::map<std::tuple<int64_t, int64_t, int64_t, int>, hipblasLtMatmulAlgo_t> algos;
+};
+std::mutex g_lt_mutex;
+LtDevice g_lt[64];
+
+// D[M,N] = A[M,K] W[K,N] (+ D when accumulate), all bf16 row-major, fp32 accumulation.  In
+// hipBLASLt's column-major terms D^T [N,M] = W^T [N,K] A^T [K,M], so W is its A operand.
+traj_status lt_gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, int64_t N, int64_t K,
+                    bool accumulate, void* ws, size_t ws_bytes, hipStream_t st) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return TRAJ_E_HIP;
+    std::lock_guard<std::mutex> lock(g_lt_mutex);
+    LtDevice& L = g_lt[dev];
+    if (L.handle == nullptr && hipblasLtCreate(&L.handle) != HIPBLAS_STATUS_SUCCESS) {
+        L.handle = nullptr;
+        return TRAJ_E_HIP;
+    }
+    hipblasLtMatmulDesc_t op = nullptr;
+    hipblasLtMatrixLayout_t lw = nullptr, la = nullptr, ld = nullptr;
+    traj_status status = TRAJ_E_HIP;
+    const hipblasOperation_t nt = HIPBLAS_OP_N;
+    do {
+        if (hipblasLtMatmulDescCreate(&op, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS) break;
+        if (hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSA, &nt, sizeof(nt)) !=
+                HIPBLAS_STATUS_SUCCESS ||
+            hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSB, &nt, sizeof(nt)) !=
+                HIPBLAS_STATUS_SUCCESS)
+            break;
+        if (hipblasLtMatrixLayoutCreate(&lw, HIP_R_16BF, N, K, N) != HIPBLAS_STATUS_SUCCESS) break;
+        if (hipblasLtMatrixLayoutCreate(&la, HIP_R_16BF, K, M, K) != HIPBLAS_STATUS_SUCCESS) break;
+        if (hipblasLtMatrixLayoutCreate(&ld, HIP_R_16BF, N, M, N) != HIPBLAS_STATUS_SUCCESS) break;
+        const auto key = std::make_tuple(M, N, K, accumulate ? 1 : 0);
+        auto it = L.algos.find(key);
+        if (it == L.algos.end()) {
+            hipblasLtMatmulPreference_t pref = nullptr;
+            if (hipblasLtMatmulPreferenceCreate(&pref) != HIPBLAS_STATUS_SUCCESS) break;
+            const uint64_t cap = ws_bytes;
+            hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &cap, sizeof(cap));
+            hipblasLtMatmulHeuristicResult_t res[1];
+            int found = 0;
+            const hipblasStatus_t hs =
+                hipblasLtMatmulAlgoGetHeuristic(L.handle, op, lw, la, ld, ld, pref, 1, res, &found);
+            hipblasLtMatmulPreferenceDestroy(pref);
+            if (hs != HIPBLAS_STATUS_SUCCESS || found < 1) break;
+            it = L.algos.emplace(key, res[0].algo).first;
+        }
+        const float alpha = 1.0f, beta = accumulate ? 1.0f : 0.0f;
+        if (hipblasLtMatmul(L.handle, op, &alpha, W, lw, A, la, &beta, D, ld, D, ld, &it->second, ws, ws_bytes, st) !=
+            HIPBLAS_STATUS_SUCCESS)
+            break;
+        status = TRAJ_OK;
+    } while (false);
+    if (ld) hipblasLtMatrixLayoutDestroy(ld);
+    if (la) hipblasLtMatrixLayoutDestroy(la);
+    if (lw) hipblasLtMatrixLayoutDestroy(lw);
+    if (op) hipblasLtMatmulDescDestroy(op);
+    return status;
+}
+
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+struct LayerPlan {
+    size_t xn, qkv, q, kd, vd, a, gu, act, lt, total;
+};
+
+LayerPlan plan_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
+    const size_t T = (size_t)sh->B * sh->N * sh->L;
+    LayerPlan p{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align256(bytes);
+        return at;
+    };
+    p.xn = take(T * dm->hidden * 2);
+    p.qkv = take(T * (size_t)(sh->Hq + 2 * sh->Hkv) * sh->D * 2);
+    p.q = take(T * (size_t)sh->Hq * sh->D * 2);
+    p.kd = take(T * (size_t)sh->Hkv * sh->D * 2);
+    p.vd = take(T * (size_t)sh->Hkv * sh->D * 2);
+    p.a = take(T * (size_t)sh->Hq * sh->D * 2);
+    p.gu = take(T * 2 * (size_t)dm->inter * 2);
+    p.act = take(T * (size_t)dm->inter * 2);
+    p.lt = take(kLtWorkspace);
+    p.total = off;
+    return p;
+}
+
+traj_status check_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
+    if (sh == nullptr || dm == nullptr) return TRAJ_E_NULL;
+    const traj_status st = check_attn(sh);
+    if (st != TRAJ_OK) return st;
+    if (dm->hidden != sh->Hq * sh->D || dm->hidden % 8 != 0 || dm->inter < 8 || dm->inter % 8 != 0) return TRAJ_E_SHAPE;
+    if (!(dm->rms_eps >= 0.f) || !(dm->rope_theta > 0.f)) return TRAJ_E_ARG;
+    return TRAJ_OK;
 }
 
 }  // namespace
@@ -286,6 +393,64 @@ traj_status traj_build_tree(const int32_t* state, const int32_t* leaf, const flo
     p.tau = threshold;
     hipLaunchKernelGGL(build_tree_kernel, dim3(p.B), dim3(kTreeThreads), 0, as_stream(stream), p);
     return launched();
+}
+
+size_t traj_verify_layer_workspace_size(const traj_attn_shape* shape, const traj_layer_dims* dims) {
+    if (check_layer(shape, dims) != TRAJ_OK) return 0;
+    return plan_layer(shape, dims).total;
+}
+
+traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_layer_dims* dims, const void* k_cache,
+                              const void* v_cache, const int32_t* draft_parent, const int32_t* pos0,
+                              const traj_attn_shape* shape, void* workspace, size_t workspace_bytes, void* stream) {
+    traj_status st = check_layer(shape, dims);
+    if (st != TRAJ_OK) return st;
+    if (x == nullptr || w == nullptr || draft_parent == nullptr || workspace == nullptr) return TRAJ_E_NULL;
+    if (w->attn_norm == nullptr || w->w_qkv == nullptr || w->w_o == nullptr || w->mlp_norm == nullptr ||
+        w->w_gate_up == nullptr || w->w_down == nullptr)
+        return TRAJ_E_NULL;
+    if (shape->S > 0 && (k_cache == nullptr || v_cache == nullptr)) return TRAJ_E_NULL;
+    if (!aligned16(x) || !aligned16(w->attn_norm) || !aligned16(w->mlp_norm) || !aligned16(w->w_qkv) ||
+        !aligned16(w->w_o) || !aligned16(w->w_gate_up) || !aligned16(w->w_down))
+        return TRAJ_E_SHAPE;
+    const LayerPlan plan = plan_layer(shape, dims);
+    if (workspace_bytes < plan.total || reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return TRAJ_E_WORKSPACE;
+    char* ws = static_cast<char*>(workspace);
+    auto buf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
+    hipStream_t s = as_stream(stream);
+    const int64_t T = (int64_t)shape->B * shape->N * shape->L;
+    const int hidden = dims->hidden, inter = dims->inter;
+    const int qkv_w = (shape->Hq + 2 * shape->Hkv) * shape->D;
+    uint16_t* xs = static_cast<uint16_t*>(x);
+    // attention block
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
+                       static_cast<const uint16_t*>(w->attn_norm), buf(plan.xn), hidden, dims->rms_eps);
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = lt_gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false,
+                      ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+        return st;
+    hipLaunchKernelGGL(rope_split_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, buf(plan.qkv), pos0,
+                       buf(plan.q), buf(plan.kd), buf(plan.vd), shape->N * shape->L, shape->L, shape->Hq, shape->Hkv,
+                       shape->D, std::log2(dims->rope_theta));
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = traj_verify_attn(buf(plan.q), k_cache, v_cache, buf(plan.kd), buf(plan.vd), draft_parent, buf(plan.a),
+                               shape, nullptr, 0, stream)) != TRAJ_OK)
+        return st;
+    if ((st = lt_gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true,
+                      ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+        return st;
+    // MLP block
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
+                       static_cast<const uint16_t*>(w->mlp_norm), buf(plan.xn), hidden, dims->rms_eps);
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = lt_gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter,
+                      hidden, false, ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+        return st;
+    hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((inter / 8 + kLayerThreads - 1) / kLayerThreads), (unsigned)T),
+                       dim3(kLayerThreads), 0, s, buf(plan.gu), buf(plan.act), inter);
+    if ((st = launched()) != TRAJ_OK) return st;
+    return lt_gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, ws + plan.lt,
+                   kLtWorkspace, s);
 }
 
 const char* traj_status_string(int32_t status) {
