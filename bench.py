@@ -291,6 +291,65 @@ def time_interblock(x, buf, tau, stream, reps=5, trig_reps=50):
             "triggered_sequences": int(out["trigger"].sum().item())}
 
 
+def time_layer(x, stream, reps=5):
+    """One verification decoder layer (traj_verify_layer) over the workload's packed drafts, with
+    random-init weights of the layer shape (MLP width 3 x hidden, as in the 8B models), and its
+    four projection GEMMs alone (traj_linear), timed with HIP events on the launch stream; not
+    part of the verification step above."""
+    wl = x.wl
+    dev = x.q.device
+    hidden, inter = wl.Hq * wl.D, 3 * wl.Hq * wl.D
+    qkv = (wl.Hq + 2 * wl.Hkv) * wl.D
+    T = wl.B * wl.N * wl.L
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed_for(wl.cid, salt=31))
+
+    def r(*shape, scale=1.0):
+        return (torch.randn(*shape, device=dev, generator=g) * scale).to(torch.bfloat16)
+
+    w = {"attn_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16), "w_qkv": r(hidden, qkv, scale=hidden ** -0.5),
+         "w_o": r(wl.Hq * wl.D, hidden, scale=hidden ** -0.5),
+         "mlp_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16),
+         "w_gate_up": r(hidden, 2 * inter, scale=hidden ** -0.5), "w_down": r(inter, hidden, scale=inter ** -0.5)}
+    h0 = r(wl.B, wl.N, wl.L, hidden)
+    h = h0.clone()
+    pos0 = torch.full((wl.B,), wl.S_prefix, dtype=torch.int32, device=dev)
+    ws = torch.empty(tsp.layer_workspace_size(wl.B, wl.N, wl.L, wl.Hq, wl.Hkv, wl.D, wl.S, hidden, inter),
+                     dtype=torch.uint8, device=dev)
+
+    def timed(fn, before=None):
+        total = 0.0
+        for i in range(reps + 1):  # the first call warms up
+            if before is not None:
+                before()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if i > 0:
+                total += e0.elapsed_time(e1)
+        return total / reps
+
+    layer_ms = timed(lambda: tsp.verify_layer(h, w, x.kc, x.vc, x.parent, wl.Hq, pos0=pos0, workspace=ws,
+                                              stream=stream), before=lambda: h.copy_(h0))
+    gemms = {}
+    a = h0.view(T, hidden)
+    for name, K, N, acc in (("qkv", hidden, qkv, False), ("o", wl.Hq * wl.D, hidden, True),
+                            ("gate_up", hidden, 2 * inter, False), ("down", inter, hidden, True)):
+        src = a if K == hidden else r(T, K)
+        y = torch.zeros(T, N, dtype=torch.bfloat16, device=dev)
+        ms = timed(lambda: tsp.linear(src, w["w_" + name], y=y, accumulate=acc, stream=stream))
+        tflops = 2.0 * T * K * N / (ms * 1e-3) / 1e12
+        gemms[name] = {"M": T, "K": K, "N": N, "ms": ms, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS}
+        del y
+    gemm_flops = 2.0 * T * hidden * (qkv + hidden + 3 * inter)
+    return {"shape": f"hidden {hidden}, {wl.Hq} q / {wl.Hkv} kv heads x {wl.D}, MLP {inter}, {T} draft tokens, "
+                     f"cache {wl.S}", "weights": "synthetic (random init)", "ms_per_layer": layer_ms,
+            "gemm_ms": sum(v["ms"] for v in gemms.values()),
+            "gemm_tflops": gemm_flops / (sum(v["ms"] for v in gemms.values()) * 1e-3) / 1e12, "gemms": gemms}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -370,6 +429,7 @@ def main():
     torch.cuda.synchronize()
     acc_main = buf.acc["n_accepted"].cpu().numpy()
     tree = None if args.no_extras else time_tree_build(x, buf, tau, stream)
+    layer = None if args.no_extras else time_layer(x, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
@@ -415,6 +475,7 @@ def main():
                 "inputs exceed the 256 MB Infinity Cache: every step reads HBM",
         "tree_build": tree,
         "interblock": inter,
+        "verify_layer": layer,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:

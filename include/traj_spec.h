@@ -20,7 +20,8 @@
  *                               (Sec. 3.4): the trigger, and attention for the joint trees of
  *                               two blocks with root-to-root visibility.
  *   6. traj_verify_layer     -- a whole decoder layer of the verification forward pass around
- *                               call 1 (norms, projections, RoPE, MLP; synthetic weights).
+ *                               call 1 (norms, projections, RoPE, MLP; synthetic weights), and
+ *                               traj_linear, its projection GEMM on its own.
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
@@ -291,13 +292,14 @@ traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int
  * by pos * rope_theta^(-2d/D), pos = pos0[b] + p for block position p of every draft (the drafts
  * are alternative states of the same block); the cache K is expected with RoPE applied.
  * Every intermediate is rounded to bf16 (the activations' storage type), arithmetic is fp32;
- * the projections are library GEMMs (hipBLASLt, fp32 accumulation).
+ * the projections are the library's own bf16 MFMA GEMM (fp32 accumulation, the residual
+ * additions fused into the O and down projections).
  * Layouts (bf16, row-major): x [B,N,L,hidden]; attn_norm, mlp_norm [hidden];
  *   w_qkv [hidden, (Hq + 2 Hkv) D]; w_o [Hq D, hidden]; w_gate_up [hidden, 2 inter] (gate then
  *   up); w_down [inter, hidden]; k_cache / v_cache and draft_parent as traj_verify_attn;
  *   pos0 [B] int32 (NULL = 0).  shape is the attention shape of the call (scale included).
- * workspace: at least traj_verify_layer_workspace_size() bytes, 256-byte aligned (all
- * intermediates plus the GEMMs' scratch).
+ * workspace: at least traj_verify_layer_workspace_size() bytes, 256-byte aligned (the
+ * intermediates: normed x, q/k/v, attention output, gate/up, activation).
  * Limits: those of traj_verify_attn; hidden == Hq * D; hidden % 8 == 0; inter % 8 == 0.
  * ------------------------------------------------------------------------------------ */
 typedef struct {
@@ -320,6 +322,17 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const 
                               const void* k_cache, const void* v_cache, const int32_t* draft_parent,
                               const int32_t* pos0, const traj_attn_shape* shape, void* workspace,
                               size_t workspace_bytes, void* stream);
+
+/* The layer's projection GEMM on its own (also the LM head of the verification forward,
+ * whose logits traj_confidence_topk reads; Sec. 3.2 "Complexity analysis"):
+ *   y[M,N] = x[M,K] @ w[K,N]            (accumulate == 0)
+ *   y[M,N] = x[M,K] @ w[K,N] + y[M,N]   (accumulate != 0; y is read, then overwritten)
+ * bf16 row-major operands, fp32 accumulation, each result rounded once to bf16 (nearest even).
+ * Limits: K and N multiples of 8 (>= 8), M >= 0 (0 = no-op), every dimension below 2^31 - 128,
+ * pointers 16-byte aligned; y must not overlap x or w.  No workspace, nothing allocated.
+ * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_NULL, TRAJ_E_HIP (launch). */
+traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_t K, int64_t N, int32_t accumulate,
+                        void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Utilities

@@ -45,7 +45,7 @@ from .accept import (  # noqa: E402
     fragile_states,
 )
 from .tree import build_tree, build_tree_batch, gather_state_scores, level_widths  # noqa: E402
-from .layer import bf16_round, verify_layer  # noqa: E402
+from .layer import bf16_round, linear, verify_layer  # noqa: E402
 from .interblock import block_top1_confidence, interblock_trigger, interblock_trigger_batch, joint_peers  # noqa: E402
 
 __all__ = [

@@ -50,6 +50,13 @@ def rope(x, pos, theta):
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
+def linear(x, w, y=None):
+    """A projection: x @ w in fp64, plus y when given (the residual add of the O and down
+    projections).  The library stores the result rounded once to bf16; this is the exact value."""
+    out = np.asarray(x, dtype=np.float64) @ np.asarray(w, dtype=np.float64)
+    return out if y is None else out + np.asarray(y, dtype=np.float64)
+
+
 def silu(g):
     return g / (1.0 + np.exp(-g))
 
@@ -71,7 +78,7 @@ def verify_layer(x, weights, k_cache, v_cache, parent, Hq, pos0=None, rms_eps=1e
 
     h = x.reshape(T, hidden)
     xn = r(rmsnorm(h, W["attn_norm"], rms_eps))
-    qkv = r(xn @ W["w_qkv"])
+    qkv = r(linear(xn, W["w_qkv"]))
     q = qkv[:, :Hq * D].reshape(T, Hq, D)
     k = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
     v = qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D)
@@ -79,9 +86,9 @@ def verify_layer(x, weights, k_cache, v_cache, parent, Hq, pos0=None, rms_eps=1e
     a = verify_attention(q.reshape(B, N, L, Hq, D), k_cache, v_cache, k.reshape(B, N, L, Hkv, D),
                          v.reshape(B, N, L, Hkv, D), parent, scale=scale)
     a = r(a).reshape(T, Hq * D)
-    h = r(h + a @ W["w_o"])
+    h = r(linear(a, W["w_o"], h))
     xn = r(rmsnorm(h, W["mlp_norm"], rms_eps))
-    gu = r(xn @ W["w_gate_up"])
+    gu = r(linear(xn, W["w_gate_up"]))
     act = r(silu(gu[:, :inter]) * gu[:, inter:])
-    h = r(h + act @ W["w_down"])
+    h = r(linear(act, W["w_down"], h))
     return h.reshape(B, N, L, hidden)

@@ -22,7 +22,8 @@ and inter-block speculation (Sec. 3.4):
   :func:`joint_peers`) verifies the joint trees with root-to-root visibility.
 
 and :func:`verify_layer`, a whole decoder layer of the verification forward pass around the
-attention (norms, projections on hipBLASLt, RoPE, SwiGLU MLP).
+attention (norms, projections on the library's MFMA GEMM, RoPE, SwiGLU MLP), and
+:func:`linear`, that GEMM on its own.
 """
 
 from ._lib import (  # noqa: F401
@@ -38,6 +39,7 @@ from ._lib import (  # noqa: F401
     interblock_trigger,
     joint_peers,
     layer_workspace_size,
+    linear,
     verify_layer,
     load,
     tree_max_nodes,

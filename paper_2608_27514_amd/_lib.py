@@ -92,6 +92,7 @@ EXPORTS = {
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                            ctypes.POINTER(AttnShape), ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]),
+    "traj_linear": (ctypes.c_int32, [ctypes.c_void_p] * 3 + [ctypes.c_int64] * 3 + [ctypes.c_int32, ctypes.c_void_p]),
     "traj_build_tree": (ctypes.c_int32, [ctypes.c_void_p] * 6 + [ctypes.POINTER(TreeShape), ctypes.c_float]
                         + [ctypes.c_void_p] * 7),
     "traj_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
@@ -363,6 +364,11 @@ def layer_workspace_size(B, N, L, Hq, Hkv, D, S, hidden, inter, rms_eps=1e-5, ro
                                                        ctypes.byref(LayerDims(hidden, inter, rms_eps, rope_theta))))
 
 
+def _expect_shape(t, name, shape):
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
 def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inter=None, rms_eps=1e-5,
                  rope_theta=500000.0, scale=0.0, workspace=None, stream=None):
     """One verification decoder layer over the packed draft tokens; updates x [B,N,L,hidden]
@@ -375,9 +381,17 @@ def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inte
     _dev(x, "x", torch.bfloat16)
     for n in LAYER_WEIGHTS:
         _dev(weights[n], n, torch.bfloat16)
+    for n, shape in (("attn_norm", (hidden,)), ("w_qkv", (hidden, (Hq + 2 * Hkv) * D)), ("w_o", (Hq * D, hidden)),
+                     ("mlp_norm", (hidden,)), ("w_gate_up", (hidden, 2 * inter)), ("w_down", (inter, hidden))):
+        _expect_shape(weights[n], n, shape)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, n, torch.bfloat16)
+        _expect_shape(t, n, (B, S, Hkv, D))
     _dev(draft_parent, "draft_parent", torch.int32)
+    _expect_shape(draft_parent, "draft_parent", (B, N))
     if pos0 is not None:
         _dev(pos0, "pos0", torch.int32)
+        _expect_shape(pos0, "pos0", (B,))
     sh = AttnShape(B, N, L, Hq, Hkv, D, S, float(scale))
     dims = LayerDims(hidden, inter, rms_eps, rope_theta)
     need = int(_lib().traj_verify_layer_workspace_size(ctypes.byref(sh), ctypes.byref(dims)))
@@ -389,6 +403,25 @@ def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inte
                                   workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "traj_verify_layer")
     return x
+
+
+def linear(x, w, y=None, accumulate=False, stream=None):
+    """y = x @ w (+ y when accumulate) for bf16 x [..., K] and w [K, N]; returns y [..., N]."""
+    _dev(x, "x", torch.bfloat16)
+    _dev(w, "w", torch.bfloat16)
+    K, N = w.shape
+    if x.shape[-1] != K:
+        raise ValueError(f"x has {x.shape[-1]} columns, w has {K} rows")
+    M = x.numel() // K
+    if y is None:
+        if accumulate:
+            raise ValueError("accumulate needs y")
+        y = torch.empty(x.shape[:-1] + (N,), dtype=torch.bfloat16, device=x.device)
+    _dev(y, "y", torch.bfloat16)
+    _expect_shape(y, "y", x.shape[:-1] + (N,))
+    _check(_lib().traj_linear(_ptr(x), _ptr(w), _ptr(y), M, K, N, 1 if accumulate else 0, _stream(stream)),
+           "traj_linear")
+    return y
 
 
 def device_status(reset=True, stream=None):

@@ -28,10 +28,6 @@ HIPCC_FLAGS = [
 ]
 
 
-# the verification layer's projections are library GEMMs
-LIBS = ["-L/opt/rocm/lib", "-lhipblaslt"]
-
-
 def hipcc_path():
     for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -46,7 +42,7 @@ def sources():
 def build(verbose=False, extra_flags=()):
     """Compile the library; always rebuilds.  Returns the library path."""
     tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc_path(), *HIPCC_FLAGS, *extra_flags, "-I", os.path.join(ROOT, "include"), *sources(), *LIBS, "-o", tmp]
+    cmd = [hipcc_path(), *HIPCC_FLAGS, *extra_flags, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

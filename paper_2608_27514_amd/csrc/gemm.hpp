@@ -1,0 +1,168 @@
+// Dense bf16 projection GEMM of the verification layer: D[M,N] = A[M,K] W[K,N] (+ D), all
+// row-major bf16, fp32 accumulation on v_mfma_f32_32x32x16_bf16, one bf16 rounding (nearest
+// even) of each result.  A holds the packed draft tokens (M = B N L rows), W a weight matrix.
+//
+// Tiling: a workgroup of 4 waves owns a 128 x 128 output tile (2 x 2 waves of 64 x 64, each
+// 2 x 2 MFMA blocks of 32 x 32) and walks K in steps of 64 through two LDS buffers: the
+// global loads of step t + 1 are in flight while step t multiplies, one barrier per step.
+//
+// Fragments: the MFMA takes 8 k-values per lane; lane half h = lane / 32 holds k = 8h .. 8h+7
+// of each 16-wide k slice, for row (A) or column (W) lane % 32.  A is k-contiguous, so an A
+// fragment is one 16-byte LDS read.  W is n-contiguous: a W fragment is two transposing
+// reads (ds_read_b64_tr_b16) of slice rows 8h .. 8h+3 and 8h+4 .. 8h+7; in each group of 16
+// lanes, lane i addresses 4 columns of row (i / 4) and receives column i of the 4 rows.
+//
+// LDS layouts (16-byte chunks permuted per row; conflict-free for each reader and writer):
+//   A tile [128][64]: chunk c of row r at c ^ ((r >> 1) & 7)   (16 rows of one chunk: 64 banks)
+//   W tile [64][128]: chunk c of row r at c ^ ((r & 3) << 2)   (4 rows x 64 bytes: 64 banks)
+//
+// Edges: N and K are multiples of 8, M is arbitrary.  A 16-byte chunk outside the matrix is
+// loaded as zeros on both operands (no contribution); stores are predicated on row < M and
+// column < N.
+#pragma once
+
+#include "common.hpp"
+
+namespace trajspec {
+
+constexpr int kGemmBM = 128;
+constexpr int kGemmBN = 128;
+constexpr int kGemmBK = 64;
+constexpr int kGemmThreads = 256;
+constexpr int kGemmAElems = kGemmBM * kGemmBK;
+constexpr int kGemmWElems = kGemmBK * kGemmBN;
+constexpr int kGemmStageElems = kGemmAElems + kGemmWElems;
+// 16-byte chunks per operand tile and thread: 1024 / 256
+constexpr int kGemmLoads = kGemmAElems / 8 / kGemmThreads;
+static_assert(kGemmWElems / 8 / kGemmThreads == kGemmLoads, "equal A and W tile loads");
+
+typedef __attribute__((address_space(3))) bf16x4_t gemm_lds_bf16x4_t;
+
+struct GemmParams {
+    const uint16_t* A;  // [M, K]
+    const uint16_t* W;  // [K, N]
+    uint16_t* D;        // [M, N]
+    int M, N, K;
+    int tiles_m;        // ceil(M / 128); the grid holds tiles_m * ceil(N / 128) workgroups
+};
+
+__device__ __forceinline__ int gemm_a_slot(int r, int c) { return r * kGemmBK + ((c ^ ((r >> 1) & 7)) << 3); }
+__device__ __forceinline__ int gemm_w_slot(int r, int c) { return r * kGemmBN + ((c ^ ((r & 3) << 2)) << 3); }
+
+template <bool ACCUMULATE>
+__global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmParams P) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * kGemmStageElems];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    // consecutive logical tiles share a W column tile and run on one XCD (one L2)
+    const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int m0 = (tile % P.tiles_m) * kGemmBM;
+    const int n0 = (tile / P.tiles_m) * kGemmBN;
+    const int M = P.M, N = P.N, K = P.K;
+
+    // loads: chunk tid + 256 j of each tile.  A: row (tid >> 3) + 32 j, chunk tid & 7.
+    // W: row (tid >> 4) + 16 j, chunk tid & 15.
+    const int a_r = tid >> 3, a_c = tid & 7;
+    const int w_r = tid >> 4, w_c = tid & 15;
+    const bool w_col_ok = n0 + 8 * w_c < N;
+    const uint16_t* a_src = P.A + (int64_t)(m0 + a_r) * K + 8 * a_c;
+    const uint16_t* w_src = P.W + (int64_t)w_r * N + n0 + 8 * w_c;
+    u32x4_t ra[kGemmLoads], rw[kGemmLoads];
+
+    auto load = [&](int t) {
+        const int k0 = t * kGemmBK;
+        const bool a_k_ok = k0 + 8 * a_c < K;
+#pragma unroll
+        for (int j = 0; j < kGemmLoads; ++j) {
+            const bool ok = a_k_ok && m0 + a_r + 32 * j < M;
+            ra[j] = ok ? *reinterpret_cast<const u32x4_t*>(a_src + (int64_t)(32 * j) * K + k0) : u32x4_t{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < kGemmLoads; ++j) {
+            const bool ok = w_col_ok && k0 + w_r + 16 * j < K;
+            rw[j] = ok ? *reinterpret_cast<const u32x4_t*>(w_src + (int64_t)(k0 + 16 * j) * N) : u32x4_t{0, 0, 0, 0};
+        }
+    };
+    auto store = [&](int buf) {
+        uint16_t* sa = lds + buf * kGemmStageElems;
+        uint16_t* sw = sa + kGemmAElems;
+#pragma unroll
+        for (int j = 0; j < kGemmLoads; ++j) *reinterpret_cast<u32x4_t*>(sa + gemm_a_slot(a_r + 32 * j, a_c)) = ra[j];
+#pragma unroll
+        for (int j = 0; j < kGemmLoads; ++j) *reinterpret_cast<u32x4_t*>(sw + gemm_w_slot(w_r + 16 * j, w_c)) = rw[j];
+    };
+
+    // fragment offsets within a stage (elements)
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r32 = lane & 31, h = lane >> 5, i16 = lane & 15, dsub = (lane >> 4) & 1;
+    int a_off[2][4];
+    int w_off[2];
+#pragma unroll
+    for (int am = 0; am < 2; ++am) {
+        const int r = wm * 64 + am * 32 + r32;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) a_off[am][kk] = gemm_a_slot(r, 2 * kk + h);
+    }
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+        const int r = 8 * h + (i16 >> 2);  // slice row; +16 kk and +4 keep r & 3
+        const int col = wn * 64 + bn * 32 + dsub * 16 + (i16 & 3) * 4;
+        w_off[bn] = kGemmAElems + gemm_w_slot(r, col >> 3) + (col & 7);
+    }
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int am = 0; am < 2; ++am)
+#pragma unroll
+        for (int bn = 0; bn < 2; ++bn) acc[am][bn] = f32x16_t{};
+
+    const int nk = (K + kGemmBK - 1) / kGemmBK;
+    load(0);
+    store(0);
+    __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+        if (t + 1 < nk) load(t + 1);
+        const uint16_t* st = lds + (t & 1) * kGemmStageElems;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            bf16x8_t af[2], bf[2];
+#pragma unroll
+            for (int am = 0; am < 2; ++am) af[am] = *reinterpret_cast<const bf16x8_t*>(st + a_off[am][kk]);
+#pragma unroll
+            for (int bn = 0; bn < 2; ++bn) {
+                const uint16_t* p = st + w_off[bn] + 16 * kk * kGemmBN;
+                const bf16x4_t b0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p));
+                const bf16x4_t b1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p + 4 * kGemmBN));
+                bf[bn] = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+            }
+#pragma unroll
+            for (int am = 0; am < 2; ++am)
+#pragma unroll
+                for (int bn = 0; bn < 2; ++bn)
+                    acc[am][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[am], bf[bn], acc[am][bn], 0, 0, 0);
+        }
+        if (t + 1 < nk) store((t + 1) & 1);
+        __syncthreads();
+    }
+
+    // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
+#pragma unroll
+    for (int am = 0; am < 2; ++am) {
+#pragma unroll
+        for (int bn = 0; bn < 2; ++bn) {
+            const int col = n0 + wn * 64 + bn * 32 + r32;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = m0 + wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                if (row < M && col < N) {
+                    uint16_t* p = P.D + (int64_t)row * N + col;
+                    float v = acc[am][bn][e];
+                    if (ACCUMULATE) v += bf16_bits_to_float(*p);
+                    *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
+                }
+            }
+        }
+    }
+}
+
+}  // namespace trajspec

@@ -2,18 +2,15 @@
 // One translation unit: the kernels live in the headers included below.
 #include <hip/hip_runtime.h>
 
-#include <hipblaslt/hipblaslt.h>
-
 #include <cmath>
-#include <map>
-#include <mutex>
-#include <tuple>
+#include <climits>
 #include <cstdint>
 
 #include "../../include/traj_spec.h"
 #include "accept.hpp"
 #include "common.hpp"
 #include "conf_topk.hpp"
+#include "gemm.hpp"
 #include "interblock.hpp"
 #include "layer.hpp"
 #include "tree.hpp"
@@ -103,73 +100,27 @@ traj_status launch_topk(const void* logits, const traj_logits_shape* sh, int k, 
 }
 
 // ------------------------------------------------------------------ verification layer
-constexpr size_t kLtWorkspace = 32u << 20;  // hipBLASLt scratch inside the layer workspace
-
-struct LtDevice {
-    hipblasLtHandle_t handle = nullptr;
-    std::map<std::tuple<int64_t, int64_t, int64_t, int>, hipblasLtMatmulAlgo_t> algos;
-};
-std::mutex g_lt_mutex;
-LtDevice g_lt[64];
-
-// D[M,N] = A[M,K] W[K,N] (+ D when accumulate), all bf16 row-major, fp32 accumulation.  In
-// hipBLASLt's column-major terms D^T [N,M] = W^T [N,K] A^T [K,M], so W is its A operand.
-traj_status lt_gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, int64_t N, int64_t K,
-                    bool accumulate, void* ws, size_t ws_bytes, hipStream_t st) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return TRAJ_E_HIP;
-    std::lock_guard<std::mutex> lock(g_lt_mutex);
-    LtDevice& L = g_lt[dev];
-    if (L.handle == nullptr && hipblasLtCreate(&L.handle) != HIPBLAS_STATUS_SUCCESS) {
-        L.handle = nullptr;
-        return TRAJ_E_HIP;
-    }
-    hipblasLtMatmulDesc_t op = nullptr;
-    hipblasLtMatrixLayout_t lw = nullptr, la = nullptr, ld = nullptr;
-    traj_status status = TRAJ_E_HIP;
-    const hipblasOperation_t nt = HIPBLAS_OP_N;
-    do {
-        if (hipblasLtMatmulDescCreate(&op, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS) break;
-        if (hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSA, &nt, sizeof(nt)) !=
-                HIPBLAS_STATUS_SUCCESS ||
-            hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSB, &nt, sizeof(nt)) !=
-                HIPBLAS_STATUS_SUCCESS)
-            break;
-        if (hipblasLtMatrixLayoutCreate(&lw, HIP_R_16BF, N, K, N) != HIPBLAS_STATUS_SUCCESS) break;
-        if (hipblasLtMatrixLayoutCreate(&la, HIP_R_16BF, K, M, K) != HIPBLAS_STATUS_SUCCESS) break;
-        if (hipblasLtMatrixLayoutCreate(&ld, HIP_R_16BF, N, M, N) != HIPBLAS_STATUS_SUCCESS) break;
-        const auto key = std::make_tuple(M, N, K, accumulate ? 1 : 0);
-        auto it = L.algos.find(key);
-        if (it == L.algos.end()) {
-            hipblasLtMatmulPreference_t pref = nullptr;
-            if (hipblasLtMatmulPreferenceCreate(&pref) != HIPBLAS_STATUS_SUCCESS) break;
-            const uint64_t cap = ws_bytes;
-            hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &cap, sizeof(cap));
-            hipblasLtMatmulHeuristicResult_t res[1];
-            int found = 0;
-            const hipblasStatus_t hs =
-                hipblasLtMatmulAlgoGetHeuristic(L.handle, op, lw, la, ld, ld, pref, 1, res, &found);
-            hipblasLtMatmulPreferenceDestroy(pref);
-            if (hs != HIPBLAS_STATUS_SUCCESS || found < 1) break;
-            it = L.algos.emplace(key, res[0].algo).first;
-        }
-        const float alpha = 1.0f, beta = accumulate ? 1.0f : 0.0f;
-        if (hipblasLtMatmul(L.handle, op, &alpha, W, lw, A, la, &beta, D, ld, D, ld, &it->second, ws, ws_bytes, st) !=
-            HIPBLAS_STATUS_SUCCESS)
-            break;
-        status = TRAJ_OK;
-    } while (false);
-    if (ld) hipblasLtMatrixLayoutDestroy(ld);
-    if (la) hipblasLtMatrixLayoutDestroy(la);
-    if (lw) hipblasLtMatrixLayoutDestroy(lw);
-    if (op) hipblasLtMatmulDescDestroy(op);
-    return status;
+// D[M,N] = A[M,K] W[K,N] (+ D when accumulate), bf16 row-major, fp32 accumulation.
+traj_status gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, int64_t N, int64_t K, bool accumulate,
+                 hipStream_t st) {
+    if (M < 1 || N < 8 || K < 8 || N % 8 != 0 || K % 8 != 0) return TRAJ_E_SHAPE;
+    if (M > INT_MAX - kGemmBM || N > INT_MAX - kGemmBN || K > INT_MAX - kGemmBK) return TRAJ_E_SHAPE;
+    if (!aligned16(A) || !aligned16(W) || !aligned16(D)) return TRAJ_E_SHAPE;
+    const int64_t tiles_m = (M + kGemmBM - 1) / kGemmBM, tiles_n = (N + kGemmBN - 1) / kGemmBN;
+    if (tiles_m * tiles_n > INT_MAX) return TRAJ_E_SHAPE;
+    const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)tiles_m};
+    const dim3 grid((unsigned)(tiles_m * tiles_n));
+    if (accumulate)
+        hipLaunchKernelGGL(gemm_bf16_kernel<true>, grid, dim3(kGemmThreads), 0, st, p);
+    else
+        hipLaunchKernelGGL(gemm_bf16_kernel<false>, grid, dim3(kGemmThreads), 0, st, p);
+    return launched();
 }
 
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct LayerPlan {
-    size_t xn, qkv, q, kd, vd, a, gu, act, lt, total;
+    size_t xn, qkv, q, kd, vd, a, gu, act, total;
 };
 
 LayerPlan plan_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
@@ -189,7 +140,6 @@ LayerPlan plan_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
     p.a = take(T * (size_t)sh->Hq * sh->D * 2);
     p.gu = take(T * 2 * (size_t)dm->inter * 2);
     p.act = take(T * (size_t)dm->inter * 2);
-    p.lt = take(kLtWorkspace);
     p.total = off;
     return p;
 }
@@ -426,8 +376,8 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_l
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
                        static_cast<const uint16_t*>(w->attn_norm), buf(plan.xn), hidden, dims->rms_eps);
     if ((st = launched()) != TRAJ_OK) return st;
-    if ((st = lt_gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false,
-                      ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false, s)) !=
+        TRAJ_OK)
         return st;
     hipLaunchKernelGGL(rope_split_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, buf(plan.qkv), pos0,
                        buf(plan.q), buf(plan.kd), buf(plan.vd), shape->N * shape->L, shape->L, shape->Hq, shape->Hkv,
@@ -436,21 +386,29 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_l
     if ((st = traj_verify_attn(buf(plan.q), k_cache, v_cache, buf(plan.kd), buf(plan.vd), draft_parent, buf(plan.a),
                                shape, nullptr, 0, stream)) != TRAJ_OK)
         return st;
-    if ((st = lt_gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true,
-                      ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+    if ((st = gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true, s)) !=
+        TRAJ_OK)
         return st;
     // MLP block
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
                        static_cast<const uint16_t*>(w->mlp_norm), buf(plan.xn), hidden, dims->rms_eps);
     if ((st = launched()) != TRAJ_OK) return st;
-    if ((st = lt_gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter,
-                      hidden, false, ws + plan.lt, kLtWorkspace, s)) != TRAJ_OK)
+    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter, hidden,
+                   false, s)) != TRAJ_OK)
         return st;
     hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((inter / 8 + kLayerThreads - 1) / kLayerThreads), (unsigned)T),
                        dim3(kLayerThreads), 0, s, buf(plan.gu), buf(plan.act), inter);
     if ((st = launched()) != TRAJ_OK) return st;
-    return lt_gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, ws + plan.lt,
-                   kLtWorkspace, s);
+    return gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, s);
+}
+
+traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_t K, int64_t N, int32_t accumulate,
+                        void* stream) {
+    if (M < 0 || K < 8 || N < 8 || K % 8 != 0 || N % 8 != 0) return TRAJ_E_SHAPE;
+    if (M == 0) return TRAJ_OK;
+    if (x == nullptr || w == nullptr || y == nullptr) return TRAJ_E_NULL;
+    return gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), static_cast<uint16_t*>(y), M, N, K,
+                accumulate != 0, as_stream(stream));
 }
 
 const char* traj_status_string(int32_t status) {

@@ -193,3 +193,33 @@ def test_joint_peers_helper_matches_oracle():
         assert [int(x) for x in got] == ref(n_cur, n_next, rc, rn)
     with pytest.raises(ValueError):
         _lib.joint_peers(60, 5)
+
+
+@needs_lib
+def test_layer_and_linear_argument_errors():
+    lib = _lib.load()
+    odd = ctypes.c_void_p(0x1008)  # 8-byte aligned only
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 0, 64, 64, 0, None) == 0     # M == 0: nothing to do
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 60, 64, 0, None) == 2     # K % 8
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 4, 0, None) == 2      # N < 8
+    assert lib.traj_linear(FAKE, FAKE, FAKE, -1, 64, 64, 0, None) == 2
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 1 << 31, 0, None) == 2
+    assert lib.traj_linear(None, FAKE, FAKE, 4, 64, 64, 0, None) == 1
+    assert lib.traj_linear(FAKE, FAKE, odd, 4, 64, 64, 1, None) == 2      # alignment
+    sh = _lib.AttnShape(1, 2, 4, 2, 2, 64, 16, 0.0)
+    assert lib.traj_verify_layer_workspace_size(ctypes.byref(sh), ctypes.byref(_lib.LayerDims(128, 256, 1e-5, 5e5))) > 0
+    for dims in (_lib.LayerDims(96, 256, 1e-5, 5e5), _lib.LayerDims(128, 12, 1e-5, 5e5),
+                 _lib.LayerDims(128, 256, -1.0, 5e5), _lib.LayerDims(128, 256, 1e-5, 0.0)):
+        assert lib.traj_verify_layer_workspace_size(ctypes.byref(sh), ctypes.byref(dims)) == 0
+    w = _lib.LayerWeights(*[0x1000] * 6)
+    dims = _lib.LayerDims(128, 256, 1e-5, 5e5)
+
+    def call(shape=sh, dm=dims, weights=w, ws_bytes=1 << 30, x=FAKE):
+        return lib.traj_verify_layer(x, ctypes.byref(weights), ctypes.byref(dm), FAKE, FAKE, FAKE, None,
+                                     ctypes.byref(shape), FAKE, ws_bytes, None)
+
+    assert call(dm=_lib.LayerDims(96, 256, 1e-5, 5e5)) == 2
+    assert call(x=None) == 1
+    assert call(weights=_lib.LayerWeights(*([0x1000] * 5 + [0]))) == 1
+    assert call(weights=_lib.LayerWeights(*([0x1000] * 5 + [0x1008]))) == 2
+    assert call(ws_bytes=16) == 5

@@ -66,3 +66,67 @@ def test_layer_is_in_place_and_reports_bad_arguments():
     small = torch.empty(1024, dtype=torch.uint8, device="cuda")
     with pytest.raises(tsp.TrajSpecError):
         tsp.verify_layer(x, w, kc, vc, par, Hq, workspace=small)
+
+
+# ---------------------------------------------------------------- the projection GEMM alone
+# The GPU accumulates bf16 products in fp32 (K / 16 dependent MFMA steps) and rounds once to
+# bf16; against the exact value: |gpu - ref| <= 2^-8 |ref| + 2^-15 (|x| @ |w| + |y0|).
+
+def _linear_bound(a, w, y0, ref):
+    mag = np.abs(a) @ np.abs(w) + (0 if y0 is None else np.abs(y0))
+    return 2.0 ** -8 * np.abs(ref) + 2.0 ** -15 * mag
+
+
+@pytest.mark.parametrize("M,K,N,acc", [
+    (1, 8, 8, False), (37, 512, 1000, False), (130, 72, 136, True), (129, 200, 264, True),
+    (256, 4096, 256, False), (300, 136, 1032, True), (5, 4104, 8, False), (128, 64, 128, True),
+])
+def test_linear_parity(M, K, N, acc):
+    rng = np.random.default_rng(M * 7 + K + N)
+    a = bf16_round(rng.standard_normal((M, K)))
+    w = bf16_round(rng.standard_normal((K, N)) / math.sqrt(K))
+    y0 = bf16_round(rng.standard_normal((M, N))) if acc else None
+    ref = oracle.linear(a, w, y0)
+    bf = lambda v: cuda(np.asarray(v, dtype=np.float32), torch.bfloat16)  # noqa: E731
+    y = bf(y0) if acc else None
+    out = tsp.linear(bf(a), bf(w), y=y, accumulate=acc)
+    torch.cuda.synchronize()
+    g = out.float().cpu().numpy().astype(np.float64)
+    assert (np.abs(g - ref) <= _linear_bound(a, w, y0, ref)).all()
+    assert np.mean(g == bf16_round(ref)) > 0.95  # mostly the correctly rounded value
+
+
+@pytest.mark.parametrize("M,K,N,acc", [
+    (3584, 4096, 12288, False),   # QKV projection, 16 sequences x W3D3 drafts (7 x 32 tokens)
+    (3584, 12288, 4096, True),    # down projection + residual
+    (32768, 4096, 12288, False),  # QKV projection, 16 sequences x 64 drafts x 32 tokens
+    (224, 4096, 126464, False),   # LM head of one sequence's W3D3 drafts
+])
+def test_linear_full_size_sampled_rows(M, K, N, acc):
+    """8B-shaped projections in the launch configuration the benchmark times; the oracle checks
+    48 sampled rows (first, last, random) in full."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(M + N)
+    a = torch.randn(M, K, device="cuda", generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, N, device="cuda", generator=g) / math.sqrt(K)).to(torch.bfloat16)
+    y0 = torch.randn(M, N, device="cuda", generator=g).to(torch.bfloat16) if acc else None
+    y = y0.clone() if acc else None
+    out = tsp.linear(a, w, y=y, accumulate=acc)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(M)
+    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 46)]))
+    ridx = torch.as_tensor(rows, device="cuda")
+    a_s = a[ridx].double().cpu().numpy()
+    w_h = w.double().cpu().numpy()
+    y_s = y0[ridx].double().cpu().numpy() if acc else None
+    ref = oracle.linear(a_s, w_h, y_s)
+    got = out[ridx].double().cpu().numpy()
+    assert (np.abs(got - ref) <= _linear_bound(a_s, w_h, y_s, ref)).all()
+
+
+def test_linear_rejects_bad_shapes():
+    x = torch.zeros(4, 60, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(tsp.TrajSpecError):
+        tsp.linear(x, torch.zeros(60, 64, dtype=torch.bfloat16, device="cuda"))
+    with pytest.raises(ValueError):
+        tsp.linear(x, torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda"))

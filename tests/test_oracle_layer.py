@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from oracle.brute import layer_scalar
-from oracle.layer import bf16_round, rmsnorm, rope, silu, verify_layer
+from oracle.layer import bf16_round, linear, rmsnorm, rope, silu, verify_layer
 
 
 def test_bf16_round_matches_torch():
@@ -47,6 +47,15 @@ def test_rope_invariants():
 def test_silu_matches_torch():
     g = np.linspace(-20, 20, 401)
     assert np.allclose(silu(g), torch.nn.functional.silu(torch.tensor(g)).numpy(), rtol=1e-14, atol=1e-300)
+
+
+def test_linear_against_loops_and_identity():
+    rng = np.random.default_rng(3)
+    x, w, y = rng.standard_normal((3, 5)), rng.standard_normal((5, 4)), rng.standard_normal((3, 4))
+    loops = [[sum(x[i][k] * w[k][j] for k in range(5)) + y[i][j] for j in range(4)] for i in range(3)]
+    assert np.allclose(linear(x, w, y), loops, rtol=1e-14, atol=1e-14)
+    assert np.array_equal(linear(x, np.eye(5)), x)
+    assert np.array_equal(linear(x, np.zeros((5, 4)), y), y)
 
 
 def _weights(rng, hidden, Hq, Hkv, D, inter, zero_out=False):
