@@ -29,6 +29,10 @@ constexpr int kGemmBM = 128;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
 constexpr int kGemmThreads = 256;
+#ifndef TRAJ_GEMM_GROUP_M
+#define TRAJ_GEMM_GROUP_M 8
+#endif
+constexpr int kGemmGroupM = TRAJ_GEMM_GROUP_M;  // row tiles per ordering group
 constexpr int kGemmAElems = kGemmBM * kGemmBK;
 constexpr int kGemmWElems = kGemmBK * kGemmBN;
 constexpr int kGemmStageElems = kGemmAElems + kGemmWElems;
@@ -43,21 +47,30 @@ struct GemmParams {
     const uint16_t* W;  // [K, N]
     uint16_t* D;        // [M, N]
     int M, N, K;
-    int tiles_m;        // ceil(M / 128); the grid holds tiles_m * ceil(N / 128) workgroups
+    int tiles_m;        // ceil(M / 128)
+    int tiles_n;        // ceil(N / 128); the grid holds tiles_m * tiles_n workgroups
 };
 
 __device__ __forceinline__ int gemm_a_slot(int r, int c) { return r * kGemmBK + ((c ^ ((r >> 1) & 7)) << 3); }
 __device__ __forceinline__ int gemm_w_slot(int r, int c) { return r * kGemmBN + ((c ^ ((r & 3) << 2)) << 3); }
 
 template <bool ACCUMULATE>
-__global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmParams P) {
+__global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * kGemmStageElems];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    // consecutive logical tiles share a W column tile and run on one XCD (one L2)
+    // Consecutive logical tiles run on one XCD (one L2) at about the same time; they are
+    // grouped kGemmGroupM row tiles x (64 / kGemmGroupM) column tiles, so A and W tiles are
+    // both reused from L2 (a plain row-major or column-major order re-reads A or W from HBM
+    // once per tile of the other operand).
     const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int m0 = (tile % P.tiles_m) * kGemmBM;
-    const int n0 = (tile / P.tiles_m) * kGemmBN;
+    const int per_group = kGemmGroupM * P.tiles_n;
+    const int group = tile / per_group;
+    const int first_m = group * kGemmGroupM;
+    const int group_m = min(P.tiles_m - first_m, kGemmGroupM);
+    const int in_group = tile - group * per_group;
+    const int m0 = (first_m + in_group % group_m) * kGemmBM;
+    const int n0 = (in_group / group_m) * kGemmBN;
     const int M = P.M, N = P.N, K = P.K;
 
     // loads: chunk tid + 256 j of each tile.  A: row (tid >> 3) + 32 j, chunk tid & 7.
@@ -154,6 +167,171 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmParams P) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int row = m0 + wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                if (row < M && col < N) {
+                    uint16_t* p = P.D + (int64_t)row * N + col;
+                    float v = acc[am][bn][e];
+                    if (ACCUMULATE) v += bf16_bits_to_float(*p);
+                    *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- 256 x 256 tiles
+// For grids that fill the chip: 8 waves (2 x 4) own a 256 x 256 tile, 128 x 64 each
+// (4 x 2 MFMA blocks, 128 fp32 accumulators per lane), so a wave reads 768 LDS bytes per MFMA
+// and the workgroup moves half the global bytes per flop of the 128 x 128 tile.  Operand
+// tiles go global -> LDS directly (buffer_load_dwordx4 ... lds, 1 KB per wave-wide load, each
+// lane fetching the chunk that the row permutation puts in its slot); loads past the matrix
+// return zeros (rows through the descriptor's size, chunks past K or N through an offset
+// beyond it).  Two 64 KB stages: step t + 1 is loaded while step t multiplies, one barrier
+// per step.  LDS layouts as above with 256-element W rows (32 chunks; the permutation only
+// touches chunk bits 2..3, so a row's chunks stay in place modulo 16).
+constexpr int kG2BM = 256;
+constexpr int kG2BN = 256;
+constexpr int kG2BK = 64;
+constexpr int kG2Waves = 8;
+constexpr int kG2Threads = kG2Waves * 64;
+constexpr int kG2AElems = kG2BM * kG2BK;               // 32 KB
+constexpr int kG2WElems = kG2BK * kG2BN;               // 32 KB
+constexpr int kG2StageElems = kG2AElems + kG2WElems;   // 64 KB
+constexpr int kG2LoadsPerWave = kG2AElems / 512 / kG2Waves;  // 1 KB wave loads per operand: 4
+static_assert(kG2WElems / 512 / kG2Waves == kG2LoadsPerWave, "equal A and W loads");
+constexpr unsigned kG2Outside = 0xFFFFFFF0u;  // a buffer offset past every descriptor's size
+// Word 3 of a raw buffer descriptor on gfx950: 32-bit data format, no swizzle.
+constexpr int kG2BufferFlags = 0x00020000;
+// s_waitcnt immediate (gfx9 encoding) for vector-memory loads only: vmcnt = 0.
+constexpr int kG2WaitVmcnt0 = 0x0F70;
+
+typedef __attribute__((address_space(3))) void gemm_lds_void_t;
+
+// Host-side choice between the two tilings.
+constexpr int64_t kGemmBigGridMin = 256;            // 256 x 256 tiles: at least one per CU
+constexpr int64_t kGemmBigMaxK = 1 << 22;           // 256 rows of A below 2^31 bytes
+constexpr int64_t kGemmBigMaxWBytes = 0xFFFFFF00u;  // all of W below the outside offset
+
+__device__ __forceinline__ int g2_w_slot(int r, int c) { return r * kG2BN + ((c ^ ((r & 3) << 2)) << 3); }
+
+template <bool ACCUMULATE>
+__global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams P) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * kG2StageElems];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int per_group = kGemmGroupM * P.tiles_n;
+    const int group = tile / per_group;
+    const int first_m = group * kGemmGroupM;
+    const int group_m = min(P.tiles_m - first_m, kGemmGroupM);
+    const int in_group = tile - group * per_group;
+    const int m0 = (first_m + in_group % group_m) * kG2BM;
+    const int n0 = (in_group / group_m) * kG2BN;
+    const int M = P.M, N = P.N, K = P.K;
+
+    // Descriptors: A from row m0 (its rows below min(M - m0, 256) are in range), W from column
+    // n0 (rows below K are in range; columns past N are sent outside explicitly).
+    const int a_rows = min(M - m0, kG2BM);
+    const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(P.A + (int64_t)m0 * K), (short)0, (int)((unsigned)a_rows * (unsigned)K * 2u), kG2BufferFlags);
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(P.W + n0), (short)0, (int)(((unsigned)K * (unsigned)N - (unsigned)n0) * 2u), kG2BufferFlags);
+
+    // This lane's load slots.  A: wave-load j fills tile rows 32 wave + 8 j .. +8; lane -> row
+    // (lane >> 3), slot chunk lane & 7, which holds logical chunk (lane & 7) ^ ((row >> 1) & 7).
+    // W: wave-load j fills tile rows 8 wave + 2 j .. +2; lane -> row (lane >> 5), slot chunk
+    // lane & 31, holding logical chunk (lane & 31) ^ ((row & 3) << 2).
+    unsigned a_off[kG2LoadsPerWave], w_off[kG2LoadsPerWave];
+    int a_kc[kG2LoadsPerWave];  // logical k of the lane's A chunk within a step
+    bool w_in[kG2LoadsPerWave];
+#pragma unroll
+    for (int j = 0; j < kG2LoadsPerWave; ++j) {
+        const int ar = 32 * wave + 8 * j + (lane >> 3);
+        const int ac = (lane & 7) ^ ((ar >> 1) & 7);
+        a_kc[j] = 8 * ac;
+        a_off[j] = (unsigned)ar * (unsigned)K * 2u + 16u * (unsigned)ac;
+        const int wr = 8 * wave + 2 * j + (lane >> 5);
+        const int wc = (lane & 31) ^ ((wr & 3) << 2);
+        w_in[j] = n0 + 8 * wc < N;
+        w_off[j] = (unsigned)wr * (unsigned)N * 2u + 16u * (unsigned)wc;
+    }
+    auto load_stage = [&](int t, uint16_t* stage) {
+        const int k0 = t * kG2BK;
+#pragma unroll
+        for (int j = 0; j < kG2LoadsPerWave; ++j) {
+            const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kG2Outside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ars, (gemm_lds_void_t*)(stage + (32 * wave + 8 * j) * kG2BK), 16,
+                                                     ao, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < kG2LoadsPerWave; ++j) {
+            const unsigned wo = w_in[j] ? w_off[j] + (unsigned)k0 * (unsigned)N * 2u : kG2Outside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wrs, (gemm_lds_void_t*)(stage + kG2AElems + (8 * wave + 2 * j) * kG2BN), 16, wo, 0, 0, 0);
+        }
+    };
+
+    // Fragment reads.  Wave (wm, wn) = (wave >> 2, wave & 3) owns rows 128 wm .. +128 and
+    // columns 64 wn .. +64.  A row r = 128 wm + 32 am + lane % 32 keeps (r >> 1) & 7 equal for
+    // every am, so the permuted chunk offset depends on kk only.
+    const int wm = wave >> 2, wn = wave & 3;
+    const int r32 = lane & 31, h = lane >> 5, i16 = lane & 15, dsub = (lane >> 4) & 1;
+    const int a_row0 = (wm * 128 + r32) * kG2BK;
+    int a_chunk[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) a_chunk[kk] = ((2 * kk + h) ^ ((r32 >> 1) & 7)) << 3;
+    int b_off[2];
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+        const int r = 8 * h + (i16 >> 2);  // +16 kk and +4 keep r & 3
+        const int col = wn * 64 + bn * 32 + dsub * 16 + (i16 & 3) * 4;
+        b_off[bn] = kG2AElems + g2_w_slot(r, col >> 3) + (col & 7);
+    }
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int am = 0; am < 4; ++am)
+#pragma unroll
+        for (int bn = 0; bn < 2; ++bn) acc[am][bn] = f32x16_t{};
+
+    const int nk = (K + kG2BK - 1) / kG2BK;
+    load_stage(0, lds);
+    __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
+    __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+        const uint16_t* st = lds + (t & 1) * kG2StageElems;
+        if (t + 1 < nk) load_stage(t + 1, lds + ((t + 1) & 1) * kG2StageElems);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            bf16x8_t af[4], bf[2];
+#pragma unroll
+            for (int am = 0; am < 4; ++am)
+                af[am] = *reinterpret_cast<const bf16x8_t*>(st + a_row0 + am * 32 * kG2BK + a_chunk[kk]);
+#pragma unroll
+            for (int bn = 0; bn < 2; ++bn) {
+                const uint16_t* p = st + b_off[bn] + 16 * kk * kG2BN;
+                const bf16x4_t b0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p));
+                const bf16x4_t b1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p + 4 * kG2BN));
+                bf[bn] = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+            }
+#pragma unroll
+            for (int am = 0; am < 4; ++am)
+#pragma unroll
+                for (int bn = 0; bn < 2; ++bn)
+                    acc[am][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[am], bf[bn], acc[am][bn], 0, 0, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
+        __syncthreads();
+    }
+
+    // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
+#pragma unroll
+    for (int am = 0; am < 4; ++am) {
+#pragma unroll
+        for (int bn = 0; bn < 2; ++bn) {
+            const int col = n0 + wn * 64 + bn * 32 + r32;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = m0 + wm * 128 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
                 if (row < M && col < N) {
                     uint16_t* p = P.D + (int64_t)row * N + col;
                     float v = acc[am][bn][e];

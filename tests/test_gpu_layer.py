@@ -80,6 +80,8 @@ def _linear_bound(a, w, y0, ref):
 @pytest.mark.parametrize("M,K,N,acc", [
     (1, 8, 8, False), (37, 512, 1000, False), (130, 72, 136, True), (129, 200, 264, True),
     (256, 4096, 256, False), (300, 136, 1032, True), (5, 4104, 8, False), (128, 64, 128, True),
+    # grids of >= 256 tiles of 256 x 256 take the large-tile kernel: ragged M, N and K edges
+    (4133, 200, 4104, False), (4133, 136, 4104, True), (4096, 8, 4096, False), (4352, 4160, 3848, True),
 ])
 def test_linear_parity(M, K, N, acc):
     rng = np.random.default_rng(M * 7 + K + N)
