@@ -215,7 +215,10 @@ __device__ __forceinline__ int g2_w_slot(int r, int c) { return r * kG2BN + ((c 
 
 template <bool ACCUMULATE>
 __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams P) {
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * kG2StageElems];
+    // Two stage buffers as separate arrays: the compiler then knows that the direct loads into
+    // one do not alias the fragment reads of the other and does not wait for them.
+    __shared__ __attribute__((aligned(1024))) uint16_t buf0[kG2StageElems];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf1[kG2StageElems];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
@@ -294,21 +297,19 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
         for (int bn = 0; bn < 2; ++bn) acc[am][bn] = f32x16_t{};
 
     const int nk = (K + kG2BK - 1) / kG2BK;
-    load_stage(0, lds);
-    __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
-    __syncthreads();
-    for (int t = 0; t < nk; ++t) {
-        const uint16_t* st = lds + (t & 1) * kG2StageElems;
-        if (t + 1 < nk) load_stage(t + 1, lds + ((t + 1) & 1) * kG2StageElems);
+    // one k step: load step t + 1 into `nxt` (if any), multiply the stage in `cur`, then wait
+    // for this wave's loads and meet at the barrier
+    auto step = [&](int t, const uint16_t* cur, uint16_t* nxt) {
+        if (t + 1 < nk) load_stage(t + 1, nxt);
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             bf16x8_t af[4], bf[2];
 #pragma unroll
             for (int am = 0; am < 4; ++am)
-                af[am] = *reinterpret_cast<const bf16x8_t*>(st + a_row0 + am * 32 * kG2BK + a_chunk[kk]);
+                af[am] = *reinterpret_cast<const bf16x8_t*>(cur + a_row0 + am * 32 * kG2BK + a_chunk[kk]);
 #pragma unroll
             for (int bn = 0; bn < 2; ++bn) {
-                const uint16_t* p = st + b_off[bn] + 16 * kk * kG2BN;
+                const uint16_t* p = cur + b_off[bn] + 16 * kk * kG2BN;
                 const bf16x4_t b0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p));
                 const bf16x4_t b1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p + 4 * kG2BN));
                 bf[bn] = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -321,6 +322,13 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
         }
         __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
         __syncthreads();
+    };
+    load_stage(0, buf0);
+    __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
+    __syncthreads();
+    for (int t = 0; t < nk; t += 2) {
+        step(t, buf0, buf1);
+        if (t + 1 < nk) step(t + 1, buf1, buf0);
     }
 
     // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
