@@ -17,8 +17,10 @@
 //   W tile [64][128]: chunk c of row r at c ^ ((r & 3) << 2)   (4 rows x 64 bytes: 64 banks)
 //
 // Edges: N and K are multiples of 8, M is arbitrary.  A 16-byte chunk outside the matrix is
-// loaded as zeros on both operands (no contribution); stores are predicated on row < M and
-// column < N.
+// loaded as zeros on both operands (no contribution).
+// Epilogue: the tile's results go through LDS (bf16, row-major) so that global reads of the old
+// D (accumulate) and the stores are whole 16-byte chunks, predicated on row < M and
+// column < N; with accumulate each result is added to the old value in fp32 and rounded once.
 #pragma once
 
 #include "common.hpp"
@@ -158,23 +160,44 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
         __syncthreads();
     }
 
+    // Epilogue through LDS (the last barrier above freed it): the output tile is staged as bf16
+    // [128][128] row-major, so global traffic is 16-byte chunks (thread tid moves chunk tid & 15
+    // of rows (tid >> 4) + 16 j).  With ACCUMULATE the old D tile is staged first and each lane
+    // adds its fp32 results to it and rounds once.
+    const int ec = tid & 15;
+    const bool col_ok = n0 + 8 * ec < N;
+    if (ACCUMULATE) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int r = (tid >> 4) + 16 * j;
+            u32x4_t v = u32x4_t{0, 0, 0, 0};
+            if (col_ok && m0 + r < M) v = *reinterpret_cast<const u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec);
+            *reinterpret_cast<u32x4_t*>(lds + r * kGemmBN + 8 * ec) = v;
+        }
+        __syncthreads();
+    }
     // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
 #pragma unroll
     for (int am = 0; am < 2; ++am) {
 #pragma unroll
         for (int bn = 0; bn < 2; ++bn) {
-            const int col = n0 + wn * 64 + bn * 32 + r32;
+            const int c = wn * 64 + bn * 32 + r32;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int row = m0 + wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-                if (row < M && col < N) {
-                    uint16_t* p = P.D + (int64_t)row * N + col;
-                    float v = acc[am][bn][e];
-                    if (ACCUMULATE) v += bf16_bits_to_float(*p);
-                    *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
-                }
+                uint16_t* p = lds + (wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3)) * kGemmBN + c;
+                float v = acc[am][bn][e];
+                if (ACCUMULATE) v += bf16_bits_to_float(*p);
+                *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
             }
         }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int r = (tid >> 4) + 16 * j;
+        if (col_ok && m0 + r < M)
+            *reinterpret_cast<u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec) =
+                *reinterpret_cast<const u32x4_t*>(lds + r * kGemmBN + 8 * ec);
     }
 }
 
@@ -331,23 +354,48 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
         if (t + 1 < nk) step(t + 1, buf1, buf0);
     }
 
+    // Epilogue through LDS (the last barrier above freed both buffers): the output tile is
+    // staged as bf16 [256][256] row-major, rows 0..127 in buf0 and 128..255 in buf1, so global
+    // traffic is 16-byte chunks (thread tid moves chunk tid & 31 of rows (tid >> 5) + 16 j).
+    // With ACCUMULATE the old D tile is staged first and each lane adds its fp32 results to it
+    // and rounds once.  Wave (wm, wn) touches only rows of buf{wm}.
+    uint16_t* half = wm == 0 ? buf0 : buf1;
+    const int ec = tid & 31;
+    const bool col_ok = n0 + 8 * ec < N;
+    if (ACCUMULATE) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int r = (tid >> 5) + 16 * j;
+            uint16_t* dst = (j < 8 ? buf0 : buf1) + (r & 127) * kG2BN + 8 * ec;
+            u32x4_t v = u32x4_t{0, 0, 0, 0};
+            if (col_ok && m0 + r < M) v = *reinterpret_cast<const u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec);
+            *reinterpret_cast<u32x4_t*>(dst) = v;
+        }
+        __syncthreads();
+    }
     // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
 #pragma unroll
     for (int am = 0; am < 4; ++am) {
 #pragma unroll
         for (int bn = 0; bn < 2; ++bn) {
-            const int col = n0 + wn * 64 + bn * 32 + r32;
+            const int c = wn * 64 + bn * 32 + r32;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int row = m0 + wm * 128 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-                if (row < M && col < N) {
-                    uint16_t* p = P.D + (int64_t)row * N + col;
-                    float v = acc[am][bn][e];
-                    if (ACCUMULATE) v += bf16_bits_to_float(*p);
-                    *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
-                }
+                uint16_t* p = half + (am * 32 + 8 * (e >> 2) + 4 * h + (e & 3)) * kG2BN + c;
+                float v = acc[am][bn][e];
+                if (ACCUMULATE) v += bf16_bits_to_float(*p);
+                *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
             }
         }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int r = (tid >> 5) + 16 * j;
+        const uint16_t* src = (j < 8 ? buf0 : buf1) + (r & 127) * kG2BN + 8 * ec;
+        if (col_ok && m0 + r < M)
+            *reinterpret_cast<u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec) =
+                *reinterpret_cast<const u32x4_t*>(src);
     }
 }
 
