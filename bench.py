@@ -291,31 +291,52 @@ def time_interblock(x, buf, tau, stream, reps=5, trig_reps=50):
             "triggered_sequences": int(out["trigger"].sum().item())}
 
 
+W3D3_PARENTS = [-1, 0, 0, 0, 1, 2, 4]  # hybrid W3D3 tree: root + 3 + 2 + 1 drafts
+
+
 def time_layer(x, stream, reps=5):
     """One verification decoder layer (traj_verify_layer) over the workload's packed drafts, with
     random-init weights of the layer shape (MLP width 3 x hidden, as in the 8B models), and its
     four projection GEMMs alone (traj_linear), timed with HIP events on the launch stream; not
     part of the verification step above."""
     wl = x.wl
-    dev = x.q.device
-    hidden, inter = wl.Hq * wl.D, 3 * wl.Hq * wl.D
-    qkv = (wl.Hq + 2 * wl.Hkv) * wl.D
-    T = wl.B * wl.N * wl.L
+    return _time_layer(wl.B, wl.N, wl.L, wl.Hq, wl.Hkv, wl.D, wl.S, wl.S_prefix, x.kc, x.vc, x.parent,
+                       seed_for(wl.cid, salt=31), stream, reps)
+
+
+def time_layer_one_sequence(wl, stream, reps=20):
+    """The same layer for one sequence's W3D3 hybrid tree (7 drafts of the block), the paper's
+    single-sequence decoding setting: 224 draft tokens, cache 512 + 224."""
+    dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
-    g.manual_seed(seed_for(wl.cid, salt=31))
+    g.manual_seed(seed_for(wl.cid, salt=37))
+    S_prefix, S = 512, 512 + 7 * wl.L
+    kc = torch.randn(1, S, wl.Hkv, wl.D, device=dev, generator=g).to(torch.bfloat16)
+    vc = torch.randn(1, S, wl.Hkv, wl.D, device=dev, generator=g).to(torch.bfloat16)
+    parent = torch.tensor([W3D3_PARENTS], dtype=torch.int32, device=dev)
+    return _time_layer(1, len(W3D3_PARENTS), wl.L, wl.Hq, wl.Hkv, wl.D, S, S_prefix, kc, vc, parent,
+                       seed_for(wl.cid, salt=41), stream, reps)
+
+
+def _time_layer(B, N, L, Hq, Hkv, D, S, S_prefix, kc, vc, parent, seed, stream, reps):
+    dev = kc.device
+    hidden, inter = Hq * D, 3 * Hq * D
+    qkv = (Hq + 2 * Hkv) * D
+    T = B * N * L
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
 
     def r(*shape, scale=1.0):
         return (torch.randn(*shape, device=dev, generator=g) * scale).to(torch.bfloat16)
 
     w = {"attn_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16), "w_qkv": r(hidden, qkv, scale=hidden ** -0.5),
-         "w_o": r(wl.Hq * wl.D, hidden, scale=hidden ** -0.5),
+         "w_o": r(Hq * D, hidden, scale=hidden ** -0.5),
          "mlp_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16),
          "w_gate_up": r(hidden, 2 * inter, scale=hidden ** -0.5), "w_down": r(inter, hidden, scale=inter ** -0.5)}
-    h0 = r(wl.B, wl.N, wl.L, hidden)
+    h0 = r(B, N, L, hidden)
     h = h0.clone()
-    pos0 = torch.full((wl.B,), wl.S_prefix, dtype=torch.int32, device=dev)
-    ws = torch.empty(tsp.layer_workspace_size(wl.B, wl.N, wl.L, wl.Hq, wl.Hkv, wl.D, wl.S, hidden, inter),
-                     dtype=torch.uint8, device=dev)
+    pos0 = torch.full((B,), S_prefix, dtype=torch.int32, device=dev)
+    ws = torch.empty(tsp.layer_workspace_size(B, N, L, Hq, Hkv, D, S, hidden, inter), dtype=torch.uint8, device=dev)
 
     def timed(fn, before=None):
         total = 0.0
@@ -331,22 +352,25 @@ def time_layer(x, stream, reps=5):
                 total += e0.elapsed_time(e1)
         return total / reps
 
-    layer_ms = timed(lambda: tsp.verify_layer(h, w, x.kc, x.vc, x.parent, wl.Hq, pos0=pos0, workspace=ws,
-                                              stream=stream), before=lambda: h.copy_(h0))
+    layer_ms = timed(lambda: tsp.verify_layer(h, w, kc, vc, parent, Hq, pos0=pos0, workspace=ws, stream=stream),
+                     before=lambda: h.copy_(h0))
     gemms = {}
     a = h0.view(T, hidden)
-    for name, K, N, acc in (("qkv", hidden, qkv, False), ("o", wl.Hq * wl.D, hidden, True),
-                            ("gate_up", hidden, 2 * inter, False), ("down", inter, hidden, True)):
+    for name, K, Nn, acc in (("qkv", hidden, qkv, False), ("o", Hq * D, hidden, True),
+                             ("gate_up", hidden, 2 * inter, False), ("down", inter, hidden, True)):
         src = a if K == hidden else r(T, K)
-        y = torch.zeros(T, N, dtype=torch.bfloat16, device=dev)
+        y = torch.zeros(T, Nn, dtype=torch.bfloat16, device=dev)
         ms = timed(lambda: tsp.linear(src, w["w_" + name], y=y, accumulate=acc, stream=stream))
-        tflops = 2.0 * T * K * N / (ms * 1e-3) / 1e12
-        gemms[name] = {"M": T, "K": K, "N": N, "ms": ms, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS}
+        tflops = 2.0 * T * K * Nn / (ms * 1e-3) / 1e12
+        weight_tbs = K * Nn * 2 / (ms * 1e-3) / 1e12
+        gemms[name] = {"M": T, "K": K, "N": Nn, "ms": ms, "tflops": tflops,
+                       "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS, "weight_read_tb_s": weight_tbs}
         del y
     gemm_flops = 2.0 * T * hidden * (qkv + hidden + 3 * inter)
-    return {"shape": f"hidden {hidden}, {wl.Hq} q / {wl.Hkv} kv heads x {wl.D}, MLP {inter}, {T} draft tokens, "
-                     f"cache {wl.S}", "weights": "synthetic (random init)", "ms_per_layer": layer_ms,
-            "gemm_ms": sum(v["ms"] for v in gemms.values()),
+    weight_bytes = 2.0 * hidden * (qkv + hidden + 3 * inter)
+    return {"shape": f"hidden {hidden}, {Hq} q / {Hkv} kv heads x {D}, MLP {inter}, {T} draft tokens, cache {S}",
+            "weights": "synthetic (random init)", "ms_per_layer": layer_ms,
+            "weight_bytes_per_layer": weight_bytes, "gemm_ms": sum(v["ms"] for v in gemms.values()),
             "gemm_tflops": gemm_flops / (sum(v["ms"] for v in gemms.values()) * 1e-3) / 1e12, "gemms": gemms}
 
 
@@ -430,6 +454,7 @@ def main():
     acc_main = buf.acc["n_accepted"].cpu().numpy()
     tree = None if args.no_extras else time_tree_build(x, buf, tau, stream)
     layer = None if args.no_extras else time_layer(x, stream)
+    layer_one = None if args.no_extras else time_layer_one_sequence(wl, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
@@ -476,6 +501,7 @@ def main():
         "tree_build": tree,
         "interblock": inter,
         "verify_layer": layer,
+        "verify_layer_one_sequence": layer_one,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:

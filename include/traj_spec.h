@@ -328,9 +328,11 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const 
  *   y[M,N] = x[M,K] @ w[K,N]            (accumulate == 0)
  *   y[M,N] = x[M,K] @ w[K,N] + y[M,N]   (accumulate != 0; y is read, then overwritten)
  * bf16 row-major operands, fp32 accumulation, each result rounded once to bf16 (nearest even).
- * Limits: K and N multiples of 8 (>= 8), M >= 0 (0 = no-op), every dimension below 2^31 - 128,
- * pointers 16-byte aligned; y must not overlap x or w.  No workspace, nothing allocated.
- * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_NULL, TRAJ_E_HIP (launch). */
+ * Limits: K and N multiples of 8 (>= 8), M >= 0 (0 = no-op) and below 2^31 - 256, pointers
+ * 16-byte aligned; y must not overlap x or w.  The kernels address operands through 32-bit
+ * buffer offsets: K <= 2^22 and N <= 2^24, else TRAJ_E_UNSUPPORTED.  No workspace, nothing
+ * allocated.
+ * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_UNSUPPORTED, TRAJ_E_NULL, TRAJ_E_HIP (launch). */
 traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_t K, int64_t N, int32_t accumulate,
                         void* stream);
 

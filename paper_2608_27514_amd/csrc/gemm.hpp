@@ -2,9 +2,9 @@
 // row-major bf16, fp32 accumulation on v_mfma_f32_32x32x16_bf16, one bf16 rounding (nearest
 // even) of each result.  A holds the packed draft tokens (M = B N L rows), W a weight matrix.
 //
-// Tiling: a workgroup of 4 waves owns a 128 x 128 output tile (2 x 2 waves of 64 x 64, each
-// 2 x 2 MFMA blocks of 32 x 32) and walks K in steps of 64 through two LDS buffers: the
-// global loads of step t + 1 are in flight while step t multiplies, one barrier per step.
+// Two tilings, chosen by the host: gemm_tile256_kernel (256 x 256 tiles, 8 waves) for grids
+// that fill the chip, gemm_ring128_kernel (128 x 128 tiles, 4 waves, a deeper stage ring)
+// for the few-sequence shapes whose k loops are latency-bound.
 //
 // Fragments: the MFMA takes 8 k-values per lane; lane half h = lane / 32 holds k = 8h .. 8h+7
 // of each 16-wide k slice, for row (A) or column (W) lane % 32.  A is k-contiguous, so an A
@@ -13,11 +13,20 @@
 // lanes, lane i addresses 4 columns of row (i / 4) and receives column i of the 4 rows.
 //
 // LDS layouts (16-byte chunks permuted per row; conflict-free for each reader and writer):
-//   A tile [128][64]: chunk c of row r at c ^ ((r >> 1) & 7)   (16 rows of one chunk: 64 banks)
-//   W tile [64][128]: chunk c of row r at c ^ ((r & 3) << 2)   (4 rows x 64 bytes: 64 banks)
+//   A stage [rows][64]: chunk c of row r at c ^ ((r >> 1) & 7)   (16 rows of one chunk: 64 banks)
+//   W stage [64][cols]: chunk c of row r at c ^ ((r & 3) << 2)   (4 rows x 64 bytes: 64 banks;
+//                       with 256 columns the permutation stays within each 16-chunk half)
 //
-// Edges: N and K are multiples of 8, M is arbitrary.  A 16-byte chunk outside the matrix is
-// loaded as zeros on both operands (no contribution).
+// Loads: operand tiles go global -> LDS directly (buffer_load_dwordx4 ... lds, 1 KB per
+// wave-wide load, each lane fetching the chunk that the row permutation puts in its slot).
+// Buffer descriptors bound A to the tile's rows and W to the rows below K; chunks past K or N
+// get an offset beyond every descriptor's size.  Out-of-range buffer loads return zeros, so
+// the edges contribute nothing.  N and K are multiples of 8, M is arbitrary.
+//
+// Tile order: consecutive logical tiles run on one XCD (one L2) at about the same time; they
+// are grouped kGemmGroupM row tiles at a time, so both A and W tiles are reused from L2 (a plain
+// row- or column-major order re-reads one operand from HBM once per tile of the other).
+//
 // Epilogue: the tile's results go through LDS (bf16, row-major) so that global reads of the old
 // D (accumulate) and the stores are whole 16-byte chunks, predicated on row < M and
 // column < N; with accumulate each result is added to the old value in fp32 and rounded once.
@@ -31,98 +40,164 @@ constexpr int kGemmBM = 128;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
 constexpr int kGemmThreads = 256;
-#ifndef TRAJ_GEMM_GROUP_M
-#define TRAJ_GEMM_GROUP_M 8
-#endif
-constexpr int kGemmGroupM = TRAJ_GEMM_GROUP_M;  // row tiles per ordering group
+constexpr int kGemmGroupM = 8;  // row tiles per ordering group
 constexpr int kGemmAElems = kGemmBM * kGemmBK;
 constexpr int kGemmWElems = kGemmBK * kGemmBN;
-constexpr int kGemmStageElems = kGemmAElems + kGemmWElems;
-// 16-byte chunks per operand tile and thread: 1024 / 256
-constexpr int kGemmLoads = kGemmAElems / 8 / kGemmThreads;
-static_assert(kGemmWElems / 8 / kGemmThreads == kGemmLoads, "equal A and W tile loads");
 
 typedef __attribute__((address_space(3))) bf16x4_t gemm_lds_bf16x4_t;
+typedef __attribute__((address_space(3))) void gemm_lds_void_t;
 
 struct GemmParams {
     const uint16_t* A;  // [M, K]
     const uint16_t* W;  // [K, N]
     uint16_t* D;        // [M, N]
     int M, N, K;
-    int tiles_m;        // ceil(M / 128)
-    int tiles_n;        // ceil(N / 128); the grid holds tiles_m * tiles_n workgroups
+    int tiles_m;        // row tiles
+    int tiles_n;        // column tiles; the grid holds tiles_m * tiles_n workgroups
 };
 
-__device__ __forceinline__ int gemm_a_slot(int r, int c) { return r * kGemmBK + ((c ^ ((r >> 1) & 7)) << 3); }
-__device__ __forceinline__ int gemm_w_slot(int r, int c) { return r * kGemmBN + ((c ^ ((r & 3) << 2)) << 3); }
+// Host-side choice between the two tilings, and the limits of their 32-bit buffer offsets.
+constexpr int64_t kGemmBigGridMin = 256;            // 256 x 256 tiles: at least one per CU
+constexpr int64_t kGemmMaxK = 1 << 22;              // 256 rows of A below 2^31 bytes
+constexpr int64_t kGemmMaxN = 1 << 24;              // 64 rows of W below 2^31 bytes
+constexpr int64_t kGemmMaxRecords = 0xFFFFFF00u;    // descriptor sizes stay below the outside offset
+constexpr unsigned kGemmOutside = 0xFFFFFFF0u;      // a buffer offset past every descriptor's size
+// Word 3 of a raw buffer descriptor on gfx950: 32-bit data format, no swizzle.
+constexpr int kGemmBufferFlags = 0x00020000;
 
-template <bool ACCUMULATE>
-__global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P) {
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * kGemmStageElems];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    // Consecutive logical tiles run on one XCD (one L2) at about the same time; they are
-    // grouped kGemmGroupM row tiles x (64 / kGemmGroupM) column tiles, so A and W tiles are
-    // both reused from L2 (a plain row-major or column-major order re-reads A or W from HBM
-    // once per tile of the other operand).
+// s_waitcnt immediate (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt at
+// their maxima) waiting until at most n vector-memory loads are outstanding.
+constexpr int wait_vmcnt_imm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
+
+// Logical tile of workgroup `bid` in the grouped, XCD-aware order.
+__device__ __forceinline__ void gemm_tile_origin(const GemmParams& P, int bm, int bn, int& m0, int& n0) {
     const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
     const int per_group = kGemmGroupM * P.tiles_n;
     const int group = tile / per_group;
     const int first_m = group * kGemmGroupM;
     const int group_m = min(P.tiles_m - first_m, kGemmGroupM);
     const int in_group = tile - group * per_group;
-    const int m0 = (first_m + in_group % group_m) * kGemmBM;
-    const int n0 = (in_group / group_m) * kGemmBN;
+    m0 = (first_m + in_group % group_m) * bm;
+    n0 = (in_group / group_m) * bn;
+}
+
+__device__ __forceinline__ int gemm_a_slot(int r, int c) { return r * kGemmBK + ((c ^ ((r >> 1) & 7)) << 3); }
+__device__ __forceinline__ int gemm_w_slot(int r, int c) { return r * kGemmBN + ((c ^ ((r & 3) << 2)) << 3); }
+
+// Raw buffer descriptor (gfx950): base address, no stride, num_records bytes, word 3 flags.
+typedef int32_t gemm_i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ gemm_i32x4_t gemm_descriptor(const void* base, unsigned num_records) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return gemm_i32x4_t{(int32_t)(uint32_t)a, (int32_t)((a >> 32) & 0xFFFFu), (int32_t)num_records, kGemmBufferFlags};
+}
+
+// ---------------------------------------------------------------- 128 x 128 tiles, stage ring
+// For grids too small to fill the chip with 256 x 256 tiles (a few sequences' drafts: M in the
+// hundreds).  There a workgroup's k loop is a chain of dependent steps, and with one stage in
+// flight each step waits a full memory latency; here K advances in steps of 64 through a ring
+// of kR1Stages LDS buffers (32 KB each), so the loads of the next kR1Stages - 1 steps are in
+// flight while a step multiplies.  4 waves (2 x 2) of 64 x 64 each (2 x 2 MFMA blocks).
+constexpr int kR1Stages = 4;
+constexpr int kR1StageElems = kGemmAElems + kGemmWElems;   // 32 KB
+constexpr int kR1Loads = kGemmAElems / 512 / 4;            // 1 KB wave loads per operand and step: 4
+static_assert(kGemmWElems / 512 / 4 == kR1Loads, "equal A and W loads");
+constexpr int kR1WaitAhead = wait_vmcnt_imm(2 * kR1Loads * (kR1Stages - 2));  // all but S - 2 steps
+static_assert(2 * kR1Loads * (kR1Stages - 2) < 64, "vmcnt has 6 bits");
+
+// One wave-wide 16-byte-per-lane load from a buffer straight into LDS (lane i -> bytes 16 i ..
+// 16 i + 15 after `lds_dst`, which must be wave-uniform).  Issued through asm so that the
+// compiler does not track it: with loads into several ring buffers outstanding, its own wait
+// insertion cannot tell which buffer they write and would wait for all of them before every
+// LDS read.  Completion is the caller's explicit s_waitcnt vmcnt; a compiler-tracked load
+// issued earlier only sees stricter waits because of these (loads complete in order).
+__device__ __forceinline__ void gemm_dma16(const gemm_i32x4_t& rsrc, unsigned voffset, uint16_t* lds_dst) {
+    const unsigned lds = __builtin_amdgcn_readfirstlane((unsigned)(size_t)((gemm_lds_void_t*)lds_dst));
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds), "v"(voffset), "s"(rsrc)
+                 : "memory", "m0");
+}
+
+// Workgroup barrier for a stage ring.  __syncthreads() carries a workgroup release fence,
+// which waits for every outstanding direct-to-LDS load and would leave one stage in flight.
+// Here each wave first waits (s_waitcnt) for exactly the loads of the stage the next step
+// reads; the bare s_barrier then makes them visible to every wave (LDS has no caches), and
+// the empty asm statements with a memory clobber keep the compiler from moving LDS reads or
+// writes across it.  Reads of a stage are consumed by MFMAs before the barrier, so they are
+// complete before any wave refills that buffer.
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <bool ACCUMULATE>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParams P) {
+    __shared__ __attribute__((aligned(1024))) uint16_t buf0[kR1StageElems];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf1[kR1StageElems];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf2[kR1StageElems];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf3[kR1StageElems];
+    static_assert(kR1Stages == 4, "the ring below is written out for four buffers");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    int m0, n0;
+    gemm_tile_origin(P, kGemmBM, kGemmBN, m0, n0);
     const int M = P.M, N = P.N, K = P.K;
 
-    // loads: chunk tid + 256 j of each tile.  A: row (tid >> 3) + 32 j, chunk tid & 7.
-    // W: row (tid >> 4) + 16 j, chunk tid & 15.
-    const int a_r = tid >> 3, a_c = tid & 7;
-    const int w_r = tid >> 4, w_c = tid & 15;
-    const bool w_col_ok = n0 + 8 * w_c < N;
-    const uint16_t* a_src = P.A + (int64_t)(m0 + a_r) * K + 8 * a_c;
-    const uint16_t* w_src = P.W + (int64_t)w_r * N + n0 + 8 * w_c;
-    u32x4_t ra[kGemmLoads], rw[kGemmLoads];
+    // A from row m0 (rows below min(M - m0, 128) in range); W one descriptor per k step, from
+    // row k0 and column n0 (rows below K in range; columns past N are sent outside explicitly)
+    const int a_rows = min(M - m0, kGemmBM);
+    const gemm_i32x4_t ars = gemm_descriptor(P.A + (int64_t)m0 * K, (unsigned)a_rows * (unsigned)K * 2u);
 
-    auto load = [&](int t) {
+    // Load slots.  A: wave-load j fills stage rows 32 wave + 8 j .. +8; lane -> row lane >> 3,
+    // slot chunk lane & 7, holding logical chunk (lane & 7) ^ ((row >> 1) & 7).  W: wave-load j
+    // fills rows 16 wave + 4 j .. +4; lane -> row lane >> 4, slot chunk lane & 15, holding
+    // logical chunk (lane & 15) ^ ((row & 3) << 2).
+    unsigned a_off[kR1Loads], w_off[kR1Loads];
+    int a_kc[kR1Loads];
+    bool w_in[kR1Loads];
+#pragma unroll
+    for (int j = 0; j < kR1Loads; ++j) {
+        const int ar = 32 * wave + 8 * j + (lane >> 3);
+        const int ac = (lane & 7) ^ ((ar >> 1) & 7);
+        a_kc[j] = 8 * ac;
+        a_off[j] = (unsigned)ar * (unsigned)K * 2u + 16u * (unsigned)ac;
+        const int wr = 16 * wave + 4 * j + (lane >> 4);
+        const int wc = (lane & 15) ^ ((wr & 3) << 2);
+        w_in[j] = n0 + 8 * wc < N;
+        w_off[j] = (unsigned)wr * (unsigned)N * 2u + 16u * (unsigned)wc;
+    }
+    auto load_stage = [&](int t, uint16_t* stage) {
         const int k0 = t * kGemmBK;
-        const bool a_k_ok = k0 + 8 * a_c < K;
+        const int64_t w_rem = ((int64_t)(K - k0) * N - n0) * 2;
+        const gemm_i32x4_t wrs = gemm_descriptor(P.W + (int64_t)k0 * N + n0, (unsigned)min(w_rem, kGemmMaxRecords));
 #pragma unroll
-        for (int j = 0; j < kGemmLoads; ++j) {
-            const bool ok = a_k_ok && m0 + a_r + 32 * j < M;
-            ra[j] = ok ? *reinterpret_cast<const u32x4_t*>(a_src + (int64_t)(32 * j) * K + k0) : u32x4_t{0, 0, 0, 0};
+        for (int j = 0; j < kR1Loads; ++j) {
+            const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
+            gemm_dma16(ars, ao, stage + (32 * wave + 8 * j) * kGemmBK);
         }
 #pragma unroll
-        for (int j = 0; j < kGemmLoads; ++j) {
-            const bool ok = w_col_ok && k0 + w_r + 16 * j < K;
-            rw[j] = ok ? *reinterpret_cast<const u32x4_t*>(w_src + (int64_t)(k0 + 16 * j) * N) : u32x4_t{0, 0, 0, 0};
+        for (int j = 0; j < kR1Loads; ++j) {
+            const unsigned wo = w_in[j] ? w_off[j] : kGemmOutside;
+            gemm_dma16(wrs, wo, stage + kGemmAElems + (16 * wave + 4 * j) * kGemmBN);
         }
-    };
-    auto store = [&](int buf) {
-        uint16_t* sa = lds + buf * kGemmStageElems;
-        uint16_t* sw = sa + kGemmAElems;
-#pragma unroll
-        for (int j = 0; j < kGemmLoads; ++j) *reinterpret_cast<u32x4_t*>(sa + gemm_a_slot(a_r + 32 * j, a_c)) = ra[j];
-#pragma unroll
-        for (int j = 0; j < kGemmLoads; ++j) *reinterpret_cast<u32x4_t*>(sw + gemm_w_slot(w_r + 16 * j, w_c)) = rw[j];
     };
 
-    // fragment offsets within a stage (elements)
     const int wm = wave >> 1, wn = wave & 1;
     const int r32 = lane & 31, h = lane >> 5, i16 = lane & 15, dsub = (lane >> 4) & 1;
-    int a_off[2][4];
-    int w_off[2];
+    int a_off_f[2][4];
+    int w_off_f[2];
 #pragma unroll
     for (int am = 0; am < 2; ++am) {
         const int r = wm * 64 + am * 32 + r32;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) a_off[am][kk] = gemm_a_slot(r, 2 * kk + h);
+        for (int kk = 0; kk < 4; ++kk) a_off_f[am][kk] = gemm_a_slot(r, 2 * kk + h);
     }
 #pragma unroll
     for (int bn = 0; bn < 2; ++bn) {
-        const int r = 8 * h + (i16 >> 2);  // slice row; +16 kk and +4 keep r & 3
+        const int r = 8 * h + (i16 >> 2);  // +16 kk and +4 keep r & 3
         const int col = wn * 64 + bn * 32 + dsub * 16 + (i16 & 3) * 4;
-        w_off[bn] = kGemmAElems + gemm_w_slot(r, col >> 3) + (col & 7);
+        w_off_f[bn] = kGemmAElems + gemm_w_slot(r, col >> 3) + (col & 7);
     }
 
     f32x16_t acc[2][2];
@@ -132,20 +207,18 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
         for (int bn = 0; bn < 2; ++bn) acc[am][bn] = f32x16_t{};
 
     const int nk = (K + kGemmBK - 1) / kGemmBK;
-    load(0);
-    store(0);
-    __syncthreads();
-    for (int t = 0; t < nk; ++t) {
-        if (t + 1 < nk) load(t + 1);
-        const uint16_t* st = lds + (t & 1) * kGemmStageElems;
+    // step t: load step t + 3 (if any) into the buffer step t - 1 read, multiply the stage in
+    // `cur`, wait until this wave's loads of step t + 1 have landed, barrier
+    auto step = [&](int t, const uint16_t* cur, uint16_t* ahead) {
+        if (t + kR1Stages - 1 < nk) load_stage(t + kR1Stages - 1, ahead);
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             bf16x8_t af[2], bf[2];
 #pragma unroll
-            for (int am = 0; am < 2; ++am) af[am] = *reinterpret_cast<const bf16x8_t*>(st + a_off[am][kk]);
+            for (int am = 0; am < 2; ++am) af[am] = *reinterpret_cast<const bf16x8_t*>(cur + a_off_f[am][kk]);
 #pragma unroll
             for (int bn = 0; bn < 2; ++bn) {
-                const uint16_t* p = st + w_off[bn] + 16 * kk * kGemmBN;
+                const uint16_t* p = cur + w_off_f[bn] + 16 * kk * kGemmBN;
                 const bf16x4_t b0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p));
                 const bf16x4_t b1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((gemm_lds_bf16x4_t*)(p + 4 * kGemmBN));
                 bf[bn] = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -156,14 +229,30 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
                 for (int bn = 0; bn < 2; ++bn)
                     acc[am][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[am], bf[bn], acc[am][bn], 0, 0, 0);
         }
-        if (t + 1 < nk) store((t + 1) & 1);
-        __syncthreads();
+        // loads issued after step t + 1's: those of steps t + 2 .. min(t + 3, nk - 1)
+        if (t + kR1Stages - 1 < nk)
+            __builtin_amdgcn_s_waitcnt(kR1WaitAhead);
+        else
+            __builtin_amdgcn_s_waitcnt(wait_vmcnt_imm(0));
+        ring_barrier();
+    };
+    load_stage(0, buf0);
+    if (1 < nk) load_stage(1, buf1);
+    if (2 < nk) load_stage(2, buf2);
+    if (kR1Stages - 1 <= nk)
+        __builtin_amdgcn_s_waitcnt(kR1WaitAhead);
+    else
+        __builtin_amdgcn_s_waitcnt(wait_vmcnt_imm(0));
+    ring_barrier();
+    for (int t0 = 0; t0 < nk; t0 += kR1Stages) {
+        step(t0, buf0, buf3);
+        if (t0 + 1 < nk) step(t0 + 1, buf1, buf0);
+        if (t0 + 2 < nk) step(t0 + 2, buf2, buf1);
+        if (t0 + 3 < nk) step(t0 + 3, buf3, buf2);
     }
 
-    // Epilogue through LDS (the last barrier above freed it): the output tile is staged as bf16
-    // [128][128] row-major, so global traffic is 16-byte chunks (thread tid moves chunk tid & 15
-    // of rows (tid >> 4) + 16 j).  With ACCUMULATE the old D tile is staged first and each lane
-    // adds its fp32 results to it and rounds once.
+    // Epilogue through LDS (buf0, freed by the last barrier), as in gemm_tile128_kernel.
+    static_assert(kGemmBM * kGemmBN <= kR1StageElems, "output tile fits one stage buffer");
     const int ec = tid & 15;
     const bool col_ok = n0 + 8 * ec < N;
     if (ACCUMULATE) {
@@ -172,11 +261,10 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
             const int r = (tid >> 4) + 16 * j;
             u32x4_t v = u32x4_t{0, 0, 0, 0};
             if (col_ok && m0 + r < M) v = *reinterpret_cast<const u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec);
-            *reinterpret_cast<u32x4_t*>(lds + r * kGemmBN + 8 * ec) = v;
+            *reinterpret_cast<u32x4_t*>(buf0 + r * kGemmBN + 8 * ec) = v;
         }
         __syncthreads();
     }
-    // acc[am][bn][e] is row 8 (e / 4) + 4 h + e % 4, column lane % 32 of its 32 x 32 block
 #pragma unroll
     for (int am = 0; am < 2; ++am) {
 #pragma unroll
@@ -184,7 +272,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
             const int c = wn * 64 + bn * 32 + r32;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                uint16_t* p = lds + (wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3)) * kGemmBN + c;
+                uint16_t* p = buf0 + (wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3)) * kGemmBN + c;
                 float v = acc[am][bn][e];
                 if (ACCUMULATE) v += bf16_bits_to_float(*p);
                 *p = __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even
@@ -197,20 +285,17 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_tile128_kernel(GemmParams P
         const int r = (tid >> 4) + 16 * j;
         if (col_ok && m0 + r < M)
             *reinterpret_cast<u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec) =
-                *reinterpret_cast<const u32x4_t*>(lds + r * kGemmBN + 8 * ec);
+                *reinterpret_cast<const u32x4_t*>(buf0 + r * kGemmBN + 8 * ec);
     }
 }
 
 // ---------------------------------------------------------------- 256 x 256 tiles
 // For grids that fill the chip: 8 waves (2 x 4) own a 256 x 256 tile, 128 x 64 each
 // (4 x 2 MFMA blocks, 128 fp32 accumulators per lane), so a wave reads 768 LDS bytes per MFMA
-// and the workgroup moves half the global bytes per flop of the 128 x 128 tile.  Operand
-// tiles go global -> LDS directly (buffer_load_dwordx4 ... lds, 1 KB per wave-wide load, each
-// lane fetching the chunk that the row permutation puts in its slot); loads past the matrix
-// return zeros (rows through the descriptor's size, chunks past K or N through an offset
-// beyond it).  Two 64 KB stages: step t + 1 is loaded while step t multiplies, one barrier
-// per step.  LDS layouts as above with 256-element W rows (32 chunks; the permutation only
-// touches chunk bits 2..3, so a row's chunks stay in place modulo 16).
+// and the workgroup moves half the global bytes per flop of the 128 x 128 tile.  Two 64 KB
+// stages: step t + 1 is loaded while step t multiplies, one barrier per step (here the direct
+// loads of this kernel are ordinary compiler-tracked builtins: with one other stage in flight,
+// in a separate LDS array, the compiler's own waits are exact).
 constexpr int kG2BM = 256;
 constexpr int kG2BN = 256;
 constexpr int kG2BK = 64;
@@ -221,18 +306,6 @@ constexpr int kG2WElems = kG2BK * kG2BN;               // 32 KB
 constexpr int kG2StageElems = kG2AElems + kG2WElems;   // 64 KB
 constexpr int kG2LoadsPerWave = kG2AElems / 512 / kG2Waves;  // 1 KB wave loads per operand: 4
 static_assert(kG2WElems / 512 / kG2Waves == kG2LoadsPerWave, "equal A and W loads");
-constexpr unsigned kG2Outside = 0xFFFFFFF0u;  // a buffer offset past every descriptor's size
-// Word 3 of a raw buffer descriptor on gfx950: 32-bit data format, no swizzle.
-constexpr int kG2BufferFlags = 0x00020000;
-// s_waitcnt immediate (gfx9 encoding) for vector-memory loads only: vmcnt = 0.
-constexpr int kG2WaitVmcnt0 = 0x0F70;
-
-typedef __attribute__((address_space(3))) void gemm_lds_void_t;
-
-// Host-side choice between the two tilings.
-constexpr int64_t kGemmBigGridMin = 256;            // 256 x 256 tiles: at least one per CU
-constexpr int64_t kGemmBigMaxK = 1 << 22;           // 256 rows of A below 2^31 bytes
-constexpr int64_t kGemmBigMaxWBytes = 0xFFFFFF00u;  // all of W below the outside offset
 
 __device__ __forceinline__ int g2_w_slot(int r, int c) { return r * kG2BN + ((c ^ ((r & 3) << 2)) << 3); }
 
@@ -244,23 +317,16 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
     __shared__ __attribute__((aligned(1024))) uint16_t buf1[kG2StageElems];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int tile = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int per_group = kGemmGroupM * P.tiles_n;
-    const int group = tile / per_group;
-    const int first_m = group * kGemmGroupM;
-    const int group_m = min(P.tiles_m - first_m, kGemmGroupM);
-    const int in_group = tile - group * per_group;
-    const int m0 = (first_m + in_group % group_m) * kG2BM;
-    const int n0 = (in_group / group_m) * kG2BN;
+    int m0, n0;
+    gemm_tile_origin(P, kG2BM, kG2BN, m0, n0);
     const int M = P.M, N = P.N, K = P.K;
 
-    // Descriptors: A from row m0 (its rows below min(M - m0, 256) are in range), W from column
-    // n0 (rows below K are in range; columns past N are sent outside explicitly).
+    // Descriptors: A from row m0 (its rows below min(M - m0, 256) are in range); W one per k
+    // step, from row k0 and column n0 (the rows below K are in range, columns past N are sent
+    // outside explicitly), so every offset stays within a step's 64 rows.
     const int a_rows = min(M - m0, kG2BM);
     const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(P.A + (int64_t)m0 * K), (short)0, (int)((unsigned)a_rows * (unsigned)K * 2u), kG2BufferFlags);
-    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(P.W + n0), (short)0, (int)(((unsigned)K * (unsigned)N - (unsigned)n0) * 2u), kG2BufferFlags);
+        (void*)(P.A + (int64_t)m0 * K), (short)0, (int)((unsigned)a_rows * (unsigned)K * 2u), kGemmBufferFlags);
 
     // This lane's load slots.  A: wave-load j fills tile rows 32 wave + 8 j .. +8; lane -> row
     // (lane >> 3), slot chunk lane & 7, which holds logical chunk (lane & 7) ^ ((row >> 1) & 7).
@@ -282,15 +348,19 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
     }
     auto load_stage = [&](int t, uint16_t* stage) {
         const int k0 = t * kG2BK;
+        const int64_t w_rem = ((int64_t)(K - k0) * N - n0) * 2;
+        const __amdgpu_buffer_rsrc_t wrs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)(P.W + (int64_t)k0 * N + n0), (short)0,
+                                              (int)(unsigned)min(w_rem, kGemmMaxRecords), kGemmBufferFlags);
 #pragma unroll
         for (int j = 0; j < kG2LoadsPerWave; ++j) {
-            const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kG2Outside;
+            const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ars, (gemm_lds_void_t*)(stage + (32 * wave + 8 * j) * kG2BK), 16,
                                                      ao, 0, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < kG2LoadsPerWave; ++j) {
-            const unsigned wo = w_in[j] ? w_off[j] + (unsigned)k0 * (unsigned)N * 2u : kG2Outside;
+            const unsigned wo = w_in[j] ? w_off[j] : kGemmOutside;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 wrs, (gemm_lds_void_t*)(stage + kG2AElems + (8 * wave + 2 * j) * kG2BN), 16, wo, 0, 0, 0);
         }
@@ -343,11 +413,11 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
                 for (int bn = 0; bn < 2; ++bn)
                     acc[am][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[am], bf[bn], acc[am][bn], 0, 0, 0);
         }
-        __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
+        __builtin_amdgcn_s_waitcnt(wait_vmcnt_imm(0));
         __syncthreads();
     };
     load_stage(0, buf0);
-    __builtin_amdgcn_s_waitcnt(kG2WaitVmcnt0);
+    __builtin_amdgcn_s_waitcnt(wait_vmcnt_imm(0));
     __syncthreads();
     for (int t = 0; t < nk; t += 2) {
         step(t, buf0, buf1);

@@ -104,12 +104,12 @@ traj_status launch_topk(const void* logits, const traj_logits_shape* sh, int k, 
 traj_status gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, int64_t N, int64_t K, bool accumulate,
                  hipStream_t st) {
     if (M < 1 || N < 8 || K < 8 || N % 8 != 0 || K % 8 != 0) return TRAJ_E_SHAPE;
-    if (M > INT_MAX - kGemmBM || N > INT_MAX - kGemmBN || K > INT_MAX - kGemmBK) return TRAJ_E_SHAPE;
+    if (M > INT_MAX - kG2BM) return TRAJ_E_SHAPE;
+    if (K > kGemmMaxK || N > kGemmMaxN) return TRAJ_E_UNSUPPORTED;  // 32-bit buffer offsets
     if (!aligned16(A) || !aligned16(W) || !aligned16(D)) return TRAJ_E_SHAPE;
-    // 256 x 256 tiles when they alone fill the chip and the operands fit the 32-bit buffer
-    // offsets of its direct loads (A: 256 rows of K; W: all of it); 128 x 128 tiles otherwise.
+    // 256 x 256 tiles when they alone fill the chip, else 128 x 128 tiles with the stage ring
     const int64_t big_m = (M + kG2BM - 1) / kG2BM, big_n = (N + kG2BN - 1) / kG2BN;
-    if (big_m * big_n >= kGemmBigGridMin && K <= kGemmBigMaxK && K * N * 2 <= (int64_t)kGemmBigMaxWBytes) {
+    if (big_m * big_n >= kGemmBigGridMin) {
         const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)big_m, (int)big_n};
         const dim3 grid((unsigned)(big_m * big_n));
         if (accumulate)
@@ -119,13 +119,12 @@ traj_status gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, i
         return launched();
     }
     const int64_t tiles_m = (M + kGemmBM - 1) / kGemmBM, tiles_n = (N + kGemmBN - 1) / kGemmBN;
-    if (tiles_m * tiles_n > INT_MAX) return TRAJ_E_SHAPE;
     const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)tiles_m, (int)tiles_n};
-    const dim3 grid((unsigned)(tiles_m * tiles_n));
+    const dim3 grid((unsigned)(tiles_m * tiles_n));  // fewer than 4 x 256 tiles
     if (accumulate)
-        hipLaunchKernelGGL(gemm_tile128_kernel<true>, grid, dim3(kGemmThreads), 0, st, p);
+        hipLaunchKernelGGL(gemm_ring128_kernel<true>, grid, dim3(kGemmThreads), 0, st, p);
     else
-        hipLaunchKernelGGL(gemm_tile128_kernel<false>, grid, dim3(kGemmThreads), 0, st, p);
+        hipLaunchKernelGGL(gemm_ring128_kernel<false>, grid, dim3(kGemmThreads), 0, st, p);
     return launched();
 }
 

@@ -203,7 +203,8 @@ def test_layer_and_linear_argument_errors():
     assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 60, 64, 0, None) == 2     # K % 8
     assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 4, 0, None) == 2      # N < 8
     assert lib.traj_linear(FAKE, FAKE, FAKE, -1, 64, 64, 0, None) == 2
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 1 << 31, 0, None) == 2
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 1 << 31, 0, None) == 4    # N past 32-bit offsets
+    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, (1 << 22) + 8, 64, 0, None) == 4
     assert lib.traj_linear(None, FAKE, FAKE, 4, 64, 64, 0, None) == 1
     assert lib.traj_linear(FAKE, FAKE, odd, 4, 64, 64, 1, None) == 2      # alignment
     sh = _lib.AttnShape(1, 2, 4, 2, 2, 64, 16, 0.0)
