@@ -360,7 +360,8 @@ def _time_layer(B, N, L, Hq, Hkv, D, S, S_prefix, kc, vc, parent, seed, stream, 
                              ("gate_up", hidden, 2 * inter, False), ("down", inter, hidden, True)):
         src = a if K == hidden else r(T, K)
         y = torch.zeros(T, Nn, dtype=torch.bfloat16, device=dev)
-        ms = timed(lambda: tsp.linear(src, w["w_" + name], y=y, accumulate=acc, stream=stream))
+        lws = torch.empty(max(tsp.linear_workspace_size(T, K, Nn), 16), dtype=torch.uint8, device=dev)
+        ms = timed(lambda: tsp.linear(src, w["w_" + name], y=y, accumulate=acc, workspace=lws, stream=stream))
         tflops = 2.0 * T * K * Nn / (ms * 1e-3) / 1e12
         weight_tbs = K * Nn * 2 / (ms * 1e-3) / 1e12
         gemms[name] = {"M": T, "K": K, "N": Nn, "ms": ms, "tflops": tflops,

@@ -299,7 +299,8 @@ traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int
  *   up); w_down [inter, hidden]; k_cache / v_cache and draft_parent as traj_verify_attn;
  *   pos0 [B] int32 (NULL = 0).  shape is the attention shape of the call (scale included).
  * workspace: at least traj_verify_layer_workspace_size() bytes, 256-byte aligned (the
- * intermediates: normed x, q/k/v, attention output, gate/up, activation).
+ * intermediates: normed x, q/k/v, attention output, gate/up, activation; and the split-K
+ * partial products of the projections for few-row shapes, as traj_linear).
  * Limits: those of traj_verify_attn; hidden == Hq * D; hidden % 8 == 0; inter % 8 == 0.
  * ------------------------------------------------------------------------------------ */
 typedef struct {
@@ -330,11 +331,18 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const 
  * bf16 row-major operands, fp32 accumulation, each result rounded once to bf16 (nearest even).
  * Limits: K and N multiples of 8 (>= 8), M >= 0 (0 = no-op) and below 2^31 - 256, pointers
  * 16-byte aligned; y must not overlap x or w.  The kernels address operands through 32-bit
- * buffer offsets: K <= 2^22 and N <= 2^24, else TRAJ_E_UNSUPPORTED.  No workspace, nothing
- * allocated.
- * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_UNSUPPORTED, TRAJ_E_NULL, TRAJ_E_HIP (launch). */
+ * buffer offsets: K <= 2^22 and N <= 2^24, else TRAJ_E_UNSUPPORTED.  Nothing is allocated.
+ * workspace (optional, may be NULL): shapes whose 128 x 128 tiles leave CUs idle (few rows:
+ * one or a few sequences' drafts) split K over several workgroups when given at least
+ * traj_linear_workspace_size(M, K, N) bytes, 16-byte aligned, for the fp32 partial products
+ * (a size of 0 means the shape is never split); with NULL the call runs unsplit.  A non-NULL
+ * workspace that is too small or misaligned is TRAJ_E_WORKSPACE.
+ * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_UNSUPPORTED, TRAJ_E_NULL, TRAJ_E_WORKSPACE,
+ * TRAJ_E_HIP (launch). */
+size_t traj_linear_workspace_size(int64_t M, int64_t K, int64_t N);
+
 traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_t K, int64_t N, int32_t accumulate,
-                        void* stream);
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Utilities

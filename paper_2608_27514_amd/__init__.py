@@ -40,6 +40,7 @@ from ._lib import (  # noqa: F401
     joint_peers,
     layer_workspace_size,
     linear,
+    linear_workspace_size,
     verify_layer,
     load,
     tree_max_nodes,

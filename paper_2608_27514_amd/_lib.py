@@ -92,7 +92,9 @@ EXPORTS = {
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                            ctypes.POINTER(AttnShape), ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]),
-    "traj_linear": (ctypes.c_int32, [ctypes.c_void_p] * 3 + [ctypes.c_int64] * 3 + [ctypes.c_int32, ctypes.c_void_p]),
+    "traj_linear_workspace_size": (ctypes.c_size_t, [ctypes.c_int64] * 3),
+    "traj_linear": (ctypes.c_int32, [ctypes.c_void_p] * 3 + [ctypes.c_int64] * 3 +
+                    [ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "traj_build_tree": (ctypes.c_int32, [ctypes.c_void_p] * 6 + [ctypes.POINTER(TreeShape), ctypes.c_float]
                         + [ctypes.c_void_p] * 7),
     "traj_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
@@ -405,8 +407,13 @@ def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inte
     return x
 
 
-def linear(x, w, y=None, accumulate=False, stream=None):
-    """y = x @ w (+ y when accumulate) for bf16 x [..., K] and w [K, N]; returns y [..., N]."""
+def linear_workspace_size(M, K, N):
+    return int(_lib().traj_linear_workspace_size(M, K, N))
+
+
+def linear(x, w, y=None, accumulate=False, workspace=None, stream=None):
+    """y = x @ w (+ y when accumulate) for bf16 x [..., K] and w [K, N]; returns y [..., N].
+    Few-row shapes split K when given a workspace (allocated here when None)."""
     _dev(x, "x", torch.bfloat16)
     _dev(w, "w", torch.bfloat16)
     K, N = w.shape
@@ -419,8 +426,12 @@ def linear(x, w, y=None, accumulate=False, stream=None):
         y = torch.empty(x.shape[:-1] + (N,), dtype=torch.bfloat16, device=x.device)
     _dev(y, "y", torch.bfloat16)
     _expect_shape(y, "y", x.shape[:-1] + (N,))
-    _check(_lib().traj_linear(_ptr(x), _ptr(w), _ptr(y), M, K, N, 1 if accumulate else 0, _stream(stream)),
-           "traj_linear")
+    if workspace is None:
+        need = linear_workspace_size(M, K, N)
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device) if need > 0 else None
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib().traj_linear(_ptr(x), _ptr(w), _ptr(y), M, K, N, 1 if accumulate else 0, _ptr(workspace), ws_bytes,
+                              _stream(stream)), "traj_linear")
     return y
 
 

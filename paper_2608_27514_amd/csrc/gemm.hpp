@@ -53,7 +53,9 @@ struct GemmParams {
     uint16_t* D;        // [M, N]
     int M, N, K;
     int tiles_m;        // row tiles
-    int tiles_n;        // column tiles; the grid holds tiles_m * tiles_n workgroups
+    int tiles_n;        // column tiles; the grid holds tiles_m * tiles_n workgroups (x)
+    float* partial;     // split-K: [splits][M][N] fp32 partial products (grid y = split)
+    int k_split;        // split-K: k per split, a multiple of 64
 };
 
 // Host-side choice between the two tilings, and the limits of their 32-bit buffer offsets.
@@ -131,7 +133,9 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <bool ACCUMULATE>
+// PARTIAL: split-K; workgroup (x, y) multiplies k in [y k_split, (y + 1) k_split) and writes its
+// fp32 products to partial[y] (gemm_split_reduce_kernel adds the splits, the old D, and rounds).
+template <bool ACCUMULATE, bool PARTIAL>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParams P) {
     __shared__ __attribute__((aligned(1024))) uint16_t buf0[kR1StageElems];
     __shared__ __attribute__((aligned(1024))) uint16_t buf1[kR1StageElems];
@@ -143,9 +147,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
     int m0, n0;
     gemm_tile_origin(P, kGemmBM, kGemmBN, m0, n0);
     const int M = P.M, N = P.N, K = P.K;
+    const int kb = PARTIAL ? (int)blockIdx.y * P.k_split : 0;  // this workgroup's k range
+    const int ke = PARTIAL ? min(K, kb + P.k_split) : K;
 
     // A from row m0 (rows below min(M - m0, 128) in range); W one descriptor per k step, from
-    // row k0 and column n0 (rows below K in range; columns past N are sent outside explicitly)
+    // row k0 and column n0 (rows below ke in range; columns past N are sent outside explicitly)
     const int a_rows = min(M - m0, kGemmBM);
     const gemm_i32x4_t ars = gemm_descriptor(P.A + (int64_t)m0 * K, (unsigned)a_rows * (unsigned)K * 2u);
 
@@ -168,12 +174,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
         w_off[j] = (unsigned)wr * (unsigned)N * 2u + 16u * (unsigned)wc;
     }
     auto load_stage = [&](int t, uint16_t* stage) {
-        const int k0 = t * kGemmBK;
-        const int64_t w_rem = ((int64_t)(K - k0) * N - n0) * 2;
+        const int k0 = kb + t * kGemmBK;
+        const int64_t w_rem = ((int64_t)(ke - k0) * N - n0) * 2;
         const gemm_i32x4_t wrs = gemm_descriptor(P.W + (int64_t)k0 * N + n0, (unsigned)min(w_rem, kGemmMaxRecords));
 #pragma unroll
         for (int j = 0; j < kR1Loads; ++j) {
-            const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
+            const unsigned ao = k0 + a_kc[j] < ke ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
             gemm_dma16(ars, ao, stage + (32 * wave + 8 * j) * kGemmBK);
         }
 #pragma unroll
@@ -206,7 +212,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
 #pragma unroll
         for (int bn = 0; bn < 2; ++bn) acc[am][bn] = f32x16_t{};
 
-    const int nk = (K + kGemmBK - 1) / kGemmBK;
+    const int nk = (ke - kb + kGemmBK - 1) / kGemmBK;
     // step t: load step t + 3 (if any) into the buffer step t - 1 read, multiply the stage in
     // `cur`, wait until this wave's loads of step t + 1 have landed, barrier
     auto step = [&](int t, const uint16_t* cur, uint16_t* ahead) {
@@ -251,7 +257,25 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
         if (t0 + 3 < nk) step(t0 + 3, buf3, buf2);
     }
 
-    // Epilogue through LDS (buf0, freed by the last barrier), as in gemm_tile128_kernel.
+    if (PARTIAL) {
+        // fp32 products straight from the accumulators: for each e, 32 lanes store 128
+        // contiguous bytes of one row
+        float* out = P.partial + (int64_t)blockIdx.y * M * N;
+#pragma unroll
+        for (int am = 0; am < 2; ++am)
+#pragma unroll
+            for (int bn = 0; bn < 2; ++bn) {
+                const int col = n0 + wn * 64 + bn * 32 + r32;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = m0 + wm * 64 + am * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                    if (row < M && col < N) out[(int64_t)row * N + col] = acc[am][bn][e];
+                }
+            }
+        return;
+    }
+
+    // Epilogue through LDS (buf0, freed by the last barrier).
     static_assert(kGemmBM * kGemmBN <= kR1StageElems, "output tile fits one stage buffer");
     const int ec = tid & 15;
     const bool col_ok = n0 + 8 * ec < N;
@@ -286,6 +310,41 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
         if (col_ok && m0 + r < M)
             *reinterpret_cast<u32x4_t*>(P.D + (int64_t)(m0 + r) * N + n0 + 8 * ec) =
                 *reinterpret_cast<const u32x4_t*>(buf0 + r * kGemmBN + 8 * ec);
+    }
+}
+
+// D = round(sum over splits of partial (+ D)), 8 columns per thread (N % 8 == 0, so a chunk
+// stays in one row); grid-stride over the M x N / 8 chunks.
+template <bool ACCUMULATE>
+__global__ __launch_bounds__(256) void gemm_split_reduce_kernel(const float* __restrict__ partial, int splits,
+                                                                uint16_t* __restrict__ D, int M, int N) {
+    const int64_t MN = (int64_t)M * N;
+    const int64_t chunks = MN / 8;
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < chunks; q += (int64_t)gridDim.x * 256) {
+        const int64_t e0 = 8 * q;
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = 0.f;
+        for (int s2 = 0; s2 < splits; ++s2) {
+            const float4 lo = *reinterpret_cast<const float4*>(partial + s2 * MN + e0);
+            const float4 hi = *reinterpret_cast<const float4*>(partial + s2 * MN + e0 + 4);
+            v[0] += lo.x; v[1] += lo.y; v[2] += lo.z; v[3] += lo.w;
+            v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
+        }
+        u32x4_t o;
+        if (ACCUMULATE) {
+            const u32x4_t d = *reinterpret_cast<const u32x4_t*>(D + e0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[2 * i] += bf16_lo(d[i]);
+                v[2 * i + 1] += bf16_hi(d[i]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            o[i] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * i]) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * i + 1]) << 16);
+        *reinterpret_cast<u32x4_t*>(D + e0) = o;
     }
 }
 

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <algorithm>
 #include <climits>
 #include <cstdint>
 
@@ -100,9 +101,38 @@ traj_status launch_topk(const void* logits, const traj_logits_shape* sh, int k, 
 }
 
 // ------------------------------------------------------------------ verification layer
-// D[M,N] = A[M,K] W[K,N] (+ D when accumulate), bf16 row-major, fp32 accumulation.
+// Split-K for grids of 128 x 128 tiles that leave CUs idle: up to kGemmMaxSplits k ranges of
+// at least kGemmMinSplitK each, so that tiles x splits stays within one workgroup per CU.
+constexpr int kGemmMaxSplits = 8;
+constexpr int64_t kGemmMinSplitK = 512;
+
+struct GemmSplit {
+    int splits;
+    int k_split;
+};
+
+GemmSplit plan_split(int64_t M, int64_t N, int64_t K) {
+    const int64_t big = ((M + kG2BM - 1) / kG2BM) * ((N + kG2BN - 1) / kG2BN);
+    const int64_t tiles = ((M + kGemmBM - 1) / kGemmBM) * ((N + kGemmBN - 1) / kGemmBN);
+    if (big >= kGemmBigGridMin || tiles >= 256) return {1, 0};
+    int64_t S = std::min<int64_t>(256 / tiles, kGemmMaxSplits);
+    while (S > 1 && K / S < kGemmMinSplitK) --S;
+    if (S <= 1) return {1, 0};
+    const int64_t k_split = ((K + S - 1) / S + kGemmBK - 1) / kGemmBK * kGemmBK;
+    return {(int)((K + k_split - 1) / k_split), (int)k_split};
+}
+
+// fp32 partial products of a split GEMM (0 when the shape is not split)
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M < 1 || N < 8 || K < 8 || K > kGemmMaxK || N > kGemmMaxN) return 0;
+    const GemmSplit sp = plan_split(M, N, K);
+    return sp.splits > 1 ? (size_t)sp.splits * (size_t)M * (size_t)N * sizeof(float) : 0;
+}
+
+// D[M,N] = A[M,K] W[K,N] (+ D when accumulate), bf16 row-major, fp32 accumulation.  `ws` (may
+// be null) holds the split-K partials when the shape is split and it is large enough.
 traj_status gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, int64_t N, int64_t K, bool accumulate,
-                 hipStream_t st) {
+                 void* ws, size_t ws_bytes, hipStream_t st) {
     if (M < 1 || N < 8 || K < 8 || N % 8 != 0 || K % 8 != 0) return TRAJ_E_SHAPE;
     if (M > INT_MAX - kG2BM) return TRAJ_E_SHAPE;
     if (K > kGemmMaxK || N > kGemmMaxN) return TRAJ_E_UNSUPPORTED;  // 32-bit buffer offsets
@@ -110,28 +140,47 @@ traj_status gemm(const uint16_t* A, const uint16_t* W, uint16_t* D, int64_t M, i
     // 256 x 256 tiles when they alone fill the chip, else 128 x 128 tiles with the stage ring
     const int64_t big_m = (M + kG2BM - 1) / kG2BM, big_n = (N + kG2BN - 1) / kG2BN;
     if (big_m * big_n >= kGemmBigGridMin) {
-        const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)big_m, (int)big_n};
+        const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)big_m, (int)big_n, nullptr, 0};
         const dim3 grid((unsigned)(big_m * big_n));
         if (accumulate)
-            hipLaunchKernelGGL(gemm_tile256_kernel<true>, grid, dim3(kG2Threads), 0, st, p);
+            hipLaunchKernelGGL((gemm_tile256_kernel<true>), grid, dim3(kG2Threads), 0, st, p);
         else
-            hipLaunchKernelGGL(gemm_tile256_kernel<false>, grid, dim3(kG2Threads), 0, st, p);
+            hipLaunchKernelGGL((gemm_tile256_kernel<false>), grid, dim3(kG2Threads), 0, st, p);
         return launched();
     }
     const int64_t tiles_m = (M + kGemmBM - 1) / kGemmBM, tiles_n = (N + kGemmBN - 1) / kGemmBN;
-    const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)tiles_m, (int)tiles_n};
     const dim3 grid((unsigned)(tiles_m * tiles_n));  // fewer than 4 x 256 tiles
+    const GemmSplit sp = plan_split(M, N, K);
+    const size_t need = gemm_workspace_bytes(M, N, K);
+    if (sp.splits > 1 && ws != nullptr && ws_bytes >= need && aligned16(ws)) {
+        const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)tiles_m, (int)tiles_n, static_cast<float*>(ws),
+                           sp.k_split};
+        hipLaunchKernelGGL((gemm_ring128_kernel<false, true>), dim3(grid.x, (unsigned)sp.splits), dim3(kGemmThreads),
+                           0, st, p);
+        traj_status rs = launched();
+        if (rs != TRAJ_OK) return rs;
+        const int64_t chunks = M * N / 8;
+        const dim3 rgrid((unsigned)std::min<int64_t>((chunks + 255) / 256, 4096));
+        if (accumulate)
+            hipLaunchKernelGGL((gemm_split_reduce_kernel<true>), rgrid, dim3(256), 0, st,
+                               static_cast<const float*>(ws), sp.splits, D, (int)M, (int)N);
+        else
+            hipLaunchKernelGGL((gemm_split_reduce_kernel<false>), rgrid, dim3(256), 0, st,
+                               static_cast<const float*>(ws), sp.splits, D, (int)M, (int)N);
+        return launched();
+    }
+    const GemmParams p{A, W, D, (int)M, (int)N, (int)K, (int)tiles_m, (int)tiles_n, nullptr, 0};
     if (accumulate)
-        hipLaunchKernelGGL(gemm_ring128_kernel<true>, grid, dim3(kGemmThreads), 0, st, p);
+        hipLaunchKernelGGL((gemm_ring128_kernel<true, false>), grid, dim3(kGemmThreads), 0, st, p);
     else
-        hipLaunchKernelGGL(gemm_ring128_kernel<false>, grid, dim3(kGemmThreads), 0, st, p);
+        hipLaunchKernelGGL((gemm_ring128_kernel<false, false>), grid, dim3(kGemmThreads), 0, st, p);
     return launched();
 }
 
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct LayerPlan {
-    size_t xn, qkv, q, kd, vd, a, gu, act, total;
+    size_t xn, qkv, q, kd, vd, a, gu, act, split, split_bytes, total;
 };
 
 LayerPlan plan_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
@@ -151,6 +200,11 @@ LayerPlan plan_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
     p.a = take(T * (size_t)sh->Hq * sh->D * 2);
     p.gu = take(T * 2 * (size_t)dm->inter * 2);
     p.act = take(T * (size_t)dm->inter * 2);
+    const int64_t hid = dm->hidden, qkv_w = (int64_t)(sh->Hq + 2 * sh->Hkv) * sh->D;
+    p.split_bytes = std::max(std::max(gemm_workspace_bytes(T, qkv_w, hid), gemm_workspace_bytes(T, hid, (int64_t)sh->Hq * sh->D)),
+                             std::max(gemm_workspace_bytes(T, 2 * (int64_t)dm->inter, hid),
+                                      gemm_workspace_bytes(T, hid, dm->inter)));
+    p.split = take(p.split_bytes);
     p.total = off;
     return p;
 }
@@ -387,8 +441,10 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_l
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
                        static_cast<const uint16_t*>(w->attn_norm), buf(plan.xn), hidden, dims->rms_eps);
     if ((st = launched()) != TRAJ_OK) return st;
-    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false, s)) !=
-        TRAJ_OK)
+    void* split = ws + plan.split;
+    const size_t split_bytes = plan.split_bytes;
+    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false, split,
+                   split_bytes, s)) != TRAJ_OK)
         return st;
     hipLaunchKernelGGL(rope_split_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, buf(plan.qkv), pos0,
                        buf(plan.q), buf(plan.kd), buf(plan.vd), shape->N * shape->L, shape->L, shape->Hq, shape->Hkv,
@@ -397,29 +453,33 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_l
     if ((st = traj_verify_attn(buf(plan.q), k_cache, v_cache, buf(plan.kd), buf(plan.vd), draft_parent, buf(plan.a),
                                shape, nullptr, 0, stream)) != TRAJ_OK)
         return st;
-    if ((st = gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true, s)) !=
-        TRAJ_OK)
+    if ((st = gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true, split,
+                   split_bytes, s)) != TRAJ_OK)
         return st;
     // MLP block
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
                        static_cast<const uint16_t*>(w->mlp_norm), buf(plan.xn), hidden, dims->rms_eps);
     if ((st = launched()) != TRAJ_OK) return st;
     if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter, hidden,
-                   false, s)) != TRAJ_OK)
+                   false, split, split_bytes, s)) != TRAJ_OK)
         return st;
     hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((inter / 8 + kLayerThreads - 1) / kLayerThreads), (unsigned)T),
                        dim3(kLayerThreads), 0, s, buf(plan.gu), buf(plan.act), inter);
     if ((st = launched()) != TRAJ_OK) return st;
-    return gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, s);
+    return gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, split, split_bytes, s);
 }
 
+size_t traj_linear_workspace_size(int64_t M, int64_t K, int64_t N) { return gemm_workspace_bytes(M, N, K); }
+
 traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_t K, int64_t N, int32_t accumulate,
-                        void* stream) {
+                        void* workspace, size_t workspace_bytes, void* stream) {
     if (M < 0 || K < 8 || N < 8 || K % 8 != 0 || N % 8 != 0) return TRAJ_E_SHAPE;
     if (M == 0) return TRAJ_OK;
     if (x == nullptr || w == nullptr || y == nullptr) return TRAJ_E_NULL;
+    if (workspace != nullptr && (workspace_bytes < gemm_workspace_bytes(M, N, K) || !aligned16(workspace)))
+        return TRAJ_E_WORKSPACE;
     return gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), static_cast<uint16_t*>(y), M, N, K,
-                accumulate != 0, as_stream(stream));
+                accumulate != 0, workspace, workspace_bytes, as_stream(stream));
 }
 
 const char* traj_status_string(int32_t status) {

@@ -199,14 +199,23 @@ def test_joint_peers_helper_matches_oracle():
 def test_layer_and_linear_argument_errors():
     lib = _lib.load()
     odd = ctypes.c_void_p(0x1008)  # 8-byte aligned only
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 0, 64, 64, 0, None) == 0     # M == 0: nothing to do
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 60, 64, 0, None) == 2     # K % 8
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 4, 0, None) == 2      # N < 8
-    assert lib.traj_linear(FAKE, FAKE, FAKE, -1, 64, 64, 0, None) == 2
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, 64, 1 << 31, 0, None) == 4    # N past 32-bit offsets
-    assert lib.traj_linear(FAKE, FAKE, FAKE, 4, (1 << 22) + 8, 64, 0, None) == 4
-    assert lib.traj_linear(None, FAKE, FAKE, 4, 64, 64, 0, None) == 1
-    assert lib.traj_linear(FAKE, FAKE, odd, 4, 64, 64, 1, None) == 2      # alignment
+    def lin(M, K, N, acc=0, x=FAKE, y=FAKE, ws=None, ws_bytes=0):
+        return lib.traj_linear(x, FAKE, y, M, K, N, acc, ws, ws_bytes, None)
+
+    assert lin(0, 64, 64) == 0                      # M == 0: nothing to do
+    assert lin(4, 60, 64) == 2                      # K % 8
+    assert lin(4, 64, 4) == 2                       # N < 8
+    assert lin(-1, 64, 64) == 2
+    assert lin(4, 64, 1 << 31) == 4                 # N past 32-bit offsets
+    assert lin(4, (1 << 22) + 8, 64) == 4
+    assert lin(4, 64, 64, x=None) == 1
+    assert lin(4, 64, 64, acc=1, y=odd) == 2        # alignment
+    need = lib.traj_linear_workspace_size(224, 12288, 4096)  # one sequence's down projection: split
+    assert need >= 224 * 4096 * 4 * 2 and need % (224 * 4096 * 4) == 0
+    assert lib.traj_linear_workspace_size(32768, 4096, 12288) == 0   # fills the chip unsplit
+    assert lib.traj_linear_workspace_size(37, 512, 1000) == 0        # too little K to split
+    assert lin(224, 12288, 4096, ws=FAKE, ws_bytes=need - 16) == 5
+    assert lin(224, 12288, 4096, ws=odd, ws_bytes=need) == 5
     sh = _lib.AttnShape(1, 2, 4, 2, 2, 64, 16, 0.0)
     assert lib.traj_verify_layer_workspace_size(ctypes.byref(sh), ctypes.byref(_lib.LayerDims(128, 256, 1e-5, 5e5))) > 0
     for dims in (_lib.LayerDims(96, 256, 1e-5, 5e5), _lib.LayerDims(128, 12, 1e-5, 5e5),

@@ -13,6 +13,7 @@ import torch
 import oracle
 import paper_2608_27514_amd as tsp
 from helpers import cuda
+from paper_2608_27514_amd import _lib
 from oracle.layer import bf16_round
 
 pytestmark = pytest.mark.gpu
@@ -29,6 +30,7 @@ def _weights(rng, hidden, Hq, Hkv, D, inter):
     (2, 4, 8, 2, 2, 128, 64, 512, [-1, 0, 0, 1]),
     (1, 7, 32, 4, 2, 64, 100, 384, [-1, 0, 0, 0, 1, 2, 4]),   # W3D3 hybrid tree, GQA, D 64
     (3, 2, 5, 1, 1, 128, 0, 136, [-1, -1]),                   # no cache, ragged sizes
+    (1, 3, 8, 8, 4, 128, 40, 3072, [-1, 0, 1]),               # few rows: split-K projections
 ])
 def test_layer_parity(B, N, L, Hq, Hkv, D, S, inter, tree):
     rng = np.random.default_rng(B * 100 + N)
@@ -82,6 +84,8 @@ def _linear_bound(a, w, y0, ref):
     (256, 4096, 256, False), (300, 136, 1032, True), (5, 4104, 8, False), (128, 64, 128, True),
     # grids of >= 256 tiles of 256 x 256 take the large-tile kernel: ragged M, N and K edges
     (4133, 200, 4104, False), (4133, 136, 4104, True), (4096, 8, 4096, False), (4352, 4160, 3848, True),
+    # few tiles: K split over workgroups (fp32 partials in the workspace, then one reduction)
+    (300, 2048, 264, True), (130, 1088, 136, True), (224, 3080, 520, False),
 ])
 def test_linear_parity(M, K, N, acc):
     rng = np.random.default_rng(M * 7 + K + N)
@@ -103,6 +107,8 @@ def test_linear_parity(M, K, N, acc):
     (3584, 12288, 4096, True),    # down projection + residual
     (32768, 4096, 12288, False),  # QKV projection, 16 sequences x 64 drafts x 32 tokens
     (224, 4096, 126464, False),   # LM head of one sequence's W3D3 drafts
+    (224, 12288, 4096, True),     # one sequence's down projection + residual (split K)
+    (224, 4096, 4096, True),      # one sequence's O projection + residual (split K)
 ])
 def test_linear_full_size_sampled_rows(M, K, N, acc):
     """8B-shaped projections in the launch configuration the benchmark times; the oracle checks
@@ -124,6 +130,30 @@ def test_linear_full_size_sampled_rows(M, K, N, acc):
     ref = oracle.linear(a_s, w_h, y_s)
     got = out[ridx].double().cpu().numpy()
     assert (np.abs(got - ref) <= _linear_bound(a_s, w_h, y_s, ref)).all()
+
+
+def test_linear_split_and_unsplit_agree():
+    """A shape that splits K runs unsplit without a workspace; both are within the bound of the
+    exact product, and the split path is the one taken with a workspace."""
+    M, K, N = 224, 12288, 4096
+    assert tsp.linear_workspace_size(M, K, N) > 0
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    a = torch.randn(M, K, device="cuda", generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, N, device="cuda", generator=g) / math.sqrt(K)).to(torch.bfloat16)
+    split = tsp.linear(a, w)
+    unsplit = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    st = _lib._lib().traj_linear(a.data_ptr(), w.data_ptr(), unsplit.data_ptr(), M, K, N, 0, None, 0,
+                                 torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    rows = np.array([0, 17, 111, 223])
+    a_s = a[torch.as_tensor(rows, device="cuda")].double().cpu().numpy()
+    w_h = w.double().cpu().numpy()
+    ref = oracle.linear(a_s, w_h)
+    for out in (split, unsplit):
+        got = out[torch.as_tensor(rows, device="cuda")].double().cpu().numpy()
+        assert (np.abs(got - ref) <= _linear_bound(a_s, w_h, None, ref)).all()
 
 
 def test_linear_rejects_bad_shapes():
