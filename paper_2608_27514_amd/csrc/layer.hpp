@@ -15,6 +15,7 @@
 namespace trajspec {
 
 constexpr int kLayerThreads = 256;
+constexpr int kLayerMaxHalf = 64;  // D / 2 for the head sizes the attention supports (64, 128)
 
 __device__ __forceinline__ uint16_t f2bf(float f) {
     return __builtin_bit_cast(uint16_t, (__bf16)f);  // round to nearest even
@@ -65,35 +66,53 @@ __global__ __launch_bounds__(kLayerThreads) void rmsnorm_kernel(const uint16_t* 
 }
 
 // qkv: [T, (Hq + 2 Hkv) D] rows [q heads | k heads | v heads]; token t = (b N + n) L + p.
-// q: [T, Hq, D], kd / vd: [T, Hkv, D].  One workgroup per token.
+// q: [T, Hq, D], kd / vd: [T, Hkv, D].  One workgroup per token: the D / 2 rotation angles
+// depend on the position only, so they are computed once per token (into LDS) for all heads;
+// every head then moves 16-byte chunks (8 elements of the first half and the matching 8 of the
+// second).  D % 16 == 0.
 __global__ __launch_bounds__(kLayerThreads) void rope_split_kernel(const uint16_t* __restrict__ qkv,
                                                                    const int32_t* __restrict__ pos0,
                                                                    uint16_t* __restrict__ q, uint16_t* __restrict__ kd,
                                                                    uint16_t* __restrict__ vd, int NL, int L, int Hq,
                                                                    int Hkv, int D, float log2_theta) {
+    __shared__ float cs[kLayerMaxHalf], sn[kLayerMaxHalf];
     const int t = blockIdx.x;
     const int b = t / NL;
     const int p = t % L;
     const float pos = (float)(pos0 != nullptr ? pos0[b] + p : p);
+    const int half = D / 2;
+    for (int d = threadIdx.x; d < half; d += kLayerThreads) {
+        const float inv_freq = exp2f(-(2.0f * d / (float)D) * log2_theta);
+        sincosf(pos * inv_freq, &sn[d], &cs[d]);
+    }
+    __syncthreads();
     const int width = (Hq + 2 * Hkv) * D;
     const uint16_t* row = qkv + (int64_t)t * width;
-    const int half = D / 2;
-    // rotated pairs of the q and k heads
-    for (int i = threadIdx.x; i < (Hq + Hkv) * half; i += kLayerThreads) {
-        const int head = i / half, d = i - head * half;
-        const float inv_freq = exp2f(-(2.0f * d / (float)D) * log2_theta);
-        float sn, cs;
-        sincosf(pos * inv_freq, &sn, &cs);
+    // rotated pairs of the q and k heads: task = (head, chunk of 8 in the first half)
+    const int cpr = half / 8;  // chunks per half
+    for (int i = threadIdx.x; i < (Hq + Hkv) * cpr; i += kLayerThreads) {
+        const int head = i / cpr, d0 = 8 * (i - head * cpr);
         const uint16_t* src = row + head * D;
-        const float x1 = bf16_bits_to_float(src[d]), x2 = bf16_bits_to_float(src[d + half]);
+        const u32x4_t a = *reinterpret_cast<const u32x4_t*>(src + d0);
+        const u32x4_t c = *reinterpret_cast<const u32x4_t*>(src + d0 + half);
+        u32x4_t lo, hi;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int d = d0 + 2 * e;
+            const float x1a = bf16_lo(a[e]), x1b = bf16_hi(a[e]);
+            const float x2a = bf16_lo(c[e]), x2b = bf16_hi(c[e]);
+            lo[e] = (uint32_t)f2bf(x1a * cs[d] - x2a * sn[d]) | ((uint32_t)f2bf(x1b * cs[d + 1] - x2b * sn[d + 1]) << 16);
+            hi[e] = (uint32_t)f2bf(x2a * cs[d] + x1a * sn[d]) | ((uint32_t)f2bf(x2b * cs[d + 1] + x1b * sn[d + 1]) << 16);
+        }
         uint16_t* dst = head < Hq ? q + ((int64_t)t * Hq + head) * D : kd + ((int64_t)t * Hkv + (head - Hq)) * D;
-        dst[d] = f2bf(x1 * cs - x2 * sn);
-        dst[d + half] = f2bf(x2 * cs + x1 * sn);
+        *reinterpret_cast<u32x4_t*>(dst + d0) = lo;
+        *reinterpret_cast<u32x4_t*>(dst + d0 + half) = hi;
     }
-    // v heads: copied
+    // v heads: copied in 16-byte chunks
     const uint16_t* vsrc = row + (Hq + Hkv) * D;
     uint16_t* vdst = vd + (int64_t)t * Hkv * D;
-    for (int i = threadIdx.x; i < Hkv * D; i += kLayerThreads) vdst[i] = vsrc[i];
+    for (int i = threadIdx.x; i < Hkv * D / 8; i += kLayerThreads)
+        *reinterpret_cast<u32x4_t*>(vdst + 8 * i) = *reinterpret_cast<const u32x4_t*>(vsrc + 8 * i);
 }
 
 // gu: [T, 2 I] rows [gate | up]; act: [T, I].  grid (ceil(I / (8 * threads)), T); I % 8 == 0.
