@@ -20,8 +20,10 @@
  *                               (Sec. 3.4): the trigger, and attention for the joint trees of
  *                               two blocks with root-to-root visibility.
  *   6. traj_verify_layer     -- a whole decoder layer of the verification forward pass around
- *                               call 1 (norms, projections, RoPE, MLP; synthetic weights), and
- *                               traj_linear, its projection GEMM on its own.
+ *                               call 1 (norms, projections, RoPE, MLP; synthetic weights),
+ *                               traj_refresh_layer, the same layer over whole sequences that
+ *                               refreshes the dual cache at a block boundary, and traj_linear,
+ *                               the projection GEMM on its own.
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller, on the device that is
@@ -64,6 +66,7 @@ typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
 /* Device status bits (traj_get_device_status). */
 #define TRAJ_DEV_BAD_PARENT 0x1 /* some parent[n] was outside [-1, n): treated as -1      */
 #define TRAJ_DEV_BAD_LEAF 0x2   /* traj_build_tree: a leaf outside [-1, n_prev): taken as -1 */
+#define TRAJ_DEV_BAD_BLOCK 0x4  /* some block_start[b] was outside [0, S]: clamped              */
 
 /* ------------------------------------------------------------------------------------
  * 1. Trajectory-masked verification attention  (Sec. 3.3; drafts packed as in Sec. 3.2
@@ -323,6 +326,32 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const 
                               const void* k_cache, const void* v_cache, const int32_t* draft_parent,
                               const int32_t* pos0, const traj_attn_shape* shape, void* workspace,
                               size_t workspace_bytes, void* stream);
+
+/* Dual-cache refresh at a block boundary (App. A: the prefix / suffix K and V the verification
+ * layer reads during a block's speculation are computed once per block, over the whole
+ * sequence).  One decoder layer, the same as traj_verify_layer's, over B whole sequences of
+ * T = S + L tokens (prefix | current block | suffix) with bidirectional attention over all T
+ * tokens of the sequence, updating x in place.  The layer's rotated K and its V of every
+ * position outside the block [block_start[b], block_start[b] + L) are written to
+ * k_cache / v_cache (prefix rows, then suffix rows): the cache traj_verify_layer takes.
+ * Positions: token t of a sequence sits at position t (block tokens at block_start + p, the
+ * positions traj_verify_layer gives the drafts with pos0 = block_start).
+ * Layouts (bf16): x [B, T, hidden]; k_cache / v_cache [B, S, Hkv, D] (written); block_start [B]
+ * int32 device array in [0, S] (a value outside is clamped and sets TRAJ_DEV_BAD_BLOCK).
+ * Weights, dims, rounding and limits as traj_verify_layer (shape->scale 0 = 1/sqrt(D)); one
+ * sequence's T K / V rows must stay below 2 GiB.
+ * workspace: at least traj_refresh_layer_workspace_size() bytes, 256-byte aligned. */
+typedef struct {
+    int32_t B, S, L, Hq, Hkv, D;
+    float scale;
+} traj_refresh_shape;
+
+size_t traj_refresh_layer_workspace_size(const traj_refresh_shape* shape, const traj_layer_dims* dims);
+
+traj_status traj_refresh_layer(void* x, const traj_layer_weights* weights, const traj_layer_dims* dims,
+                               const int32_t* block_start, void* k_cache, void* v_cache,
+                               const traj_refresh_shape* shape, void* workspace, size_t workspace_bytes,
+                               void* stream);
 
 /* The layer's projection GEMM on its own (also the LM head of the verification forward,
  * whose logits traj_confidence_topk reads; Sec. 3.2 "Complexity analysis"):

@@ -18,7 +18,8 @@ Decoding for Diffusion LLMs):
 * :mod:`oracle.interblock` -- inter-block speculation trigger and the joint
   tree's root-to-root visibility (Sec. 3.4, App. D).
 * :mod:`oracle.layer`      -- one verification decoder layer around the attention
-  (RMSNorm, projections, rotary positions, SwiGLU MLP) with bf16 storage.
+  (RMSNorm, projections, rotary positions, SwiGLU MLP) with bf16 storage, and the
+  same layer over whole sequences that refreshes the dual cache (App. A).
 * :mod:`oracle.brute`      -- scalar-loop re-derivations used only to pin the
   functions above on tiny inputs.
 
@@ -45,7 +46,7 @@ from .accept import (  # noqa: E402
     fragile_states,
 )
 from .tree import build_tree, build_tree_batch, gather_state_scores, level_widths  # noqa: E402
-from .layer import bf16_round, linear, verify_layer  # noqa: E402
+from .layer import bf16_round, full_attention, linear, refresh_layer, verify_layer  # noqa: E402
 from .interblock import block_top1_confidence, interblock_trigger, interblock_trigger_batch, joint_peers  # noqa: E402
 
 __all__ = [

@@ -1,4 +1,5 @@
-"""Oracle: one verification decoder layer around the trajectory-masked attention.
+"""Oracle: one verification decoder layer around the trajectory-masked attention, and the
+dual-cache refresh layer.
 
 TEST INFRASTRUCTURE ONLY -- see the package docstring.
 
@@ -18,6 +19,13 @@ supplies the rest).  One pre-norm decoder layer of the 8B-shaped diffusion LMs t
   of the same block, Sec. 3.2 "Tree construction").
 * Arithmetic in fp64; values are rounded to bf16 (round to nearest even, through fp32) wherever
   the library stores an activation, so that both sides see the same stored intermediates.
+
+Dual-cache refresh (App. A): at a block boundary the model runs over the whole sequence
+(prefix, the block, suffix: T = S + L tokens at positions 0 .. T-1) with bidirectional
+attention, and the K / V of the prefix and suffix positions are kept as the cache for the
+block's speculation.  :func:`refresh_layer` is the same decoder layer as above over whole
+sequences, with full attention in place of the trajectory mask, returning that cache (the
+rotated K, as the verification layer expects it).
 """
 
 import numpy as np
@@ -92,3 +100,54 @@ def verify_layer(x, weights, k_cache, v_cache, parent, Hq, pos0=None, rms_eps=1e
     act = r(silu(gu[:, :inter]) * gu[:, inter:])
     h = r(linear(act, W["w_down"], h))
     return h.reshape(B, N, L, hidden)
+
+
+def full_attention(q, k, v, scale=None):
+    """Bidirectional attention of one sequence: q [T, Hq, D], k / v [T2, Hkv, D]; query head h
+    reads K / V head h // (Hq / Hkv).  softmax(q k^T * scale) v per head, fp64."""
+    q, k, v = (np.asarray(a, dtype=np.float64) for a in (q, k, v))
+    T, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    out = np.empty((T, Hq, D))
+    for h in range(Hq):
+        s = q[:, h] @ k[:, h // G].T * scale
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        out[:, h] = (p / p.sum(axis=1, keepdims=True)) @ v[:, h // G]
+    return out
+
+
+def refresh_layer(x, weights, block_start, L, Hq, Hkv, rms_eps=1e-5, rope_theta=500000.0, scale=None):
+    """x [B, T, hidden] (bf16 values), block_start [B] in [0, T - L].  Returns the updated x and
+    the cache (k_cache, v_cache) [B, S, Hkv, D] of the positions outside each block (prefix
+    rows, then suffix rows), all float64 holding bf16 values."""
+    r = bf16_round
+    x = np.asarray(x, dtype=np.float64)
+    B, T, hidden = x.shape
+    D = hidden // Hq
+    S = T - L
+    W = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
+    inter = W["w_down"].shape[0]
+    out = np.empty_like(x)
+    k_cache = np.empty((B, S, Hkv, D))
+    v_cache = np.empty((B, S, Hkv, D))
+    pos = np.arange(T)
+    for b in range(B):
+        h = x[b]
+        xn = r(rmsnorm(h, W["attn_norm"], rms_eps))
+        qkv = r(linear(xn, W["w_qkv"]))
+        q = qkv[:, :Hq * D].reshape(T, Hq, D)
+        k = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
+        v = qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D)
+        q, k = r(rope(q, pos, rope_theta)), r(rope(k, pos, rope_theta))
+        bs = int(block_start[b])
+        keep = np.r_[0:bs, bs + L:T]  # prefix then suffix
+        k_cache[b], v_cache[b] = k[keep], v[keep]
+        a = r(full_attention(q, k, v, scale)).reshape(T, Hq * D)
+        h = r(linear(a, W["w_o"], h))
+        xn = r(rmsnorm(h, W["mlp_norm"], rms_eps))
+        gu = r(linear(xn, W["w_gate_up"]))
+        act = r(silu(gu[:, :inter]) * gu[:, inter:])
+        out[b] = r(linear(act, W["w_down"], h))
+    return out, k_cache, v_cache

@@ -23,10 +23,12 @@ and inter-block speculation (Sec. 3.4):
 
 and :func:`verify_layer`, a whole decoder layer of the verification forward pass around the
 attention (norms, projections on the library's MFMA GEMM, RoPE, SwiGLU MLP), and
-:func:`linear`, that GEMM on its own.
+:func:`linear`, that GEMM on its own; :func:`refresh_layer` runs the same layer over whole
+sequences at a block boundary and refreshes the dual cache (App. A).
 """
 
 from ._lib import (  # noqa: F401
+    DEV_BAD_BLOCK,
     DEV_BAD_LEAF,
     DEV_BAD_PARENT,
     LIB_PATH,
@@ -41,6 +43,8 @@ from ._lib import (  # noqa: F401
     layer_workspace_size,
     linear,
     linear_workspace_size,
+    refresh_layer,
+    refresh_layer_workspace_size,
     verify_layer,
     load,
     tree_max_nodes,

@@ -23,6 +23,7 @@ MODES = {"exact": 0, "top1": 1, "topk": 2}
 TRAVERSALS = {"greedy": 0, "longest": 1}
 DEV_BAD_PARENT = 0x1
 DEV_BAD_LEAF = 0x2
+DEV_BAD_BLOCK = 0x4
 
 
 class TrajSpecError(RuntimeError):
@@ -65,6 +66,11 @@ class LayerDims(ctypes.Structure):
                 ("rope_theta", ctypes.c_float)]
 
 
+class RefreshShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("S", ctypes.c_int32), ("L", ctypes.c_int32), ("Hq", ctypes.c_int32),
+                ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
 
@@ -88,6 +94,11 @@ EXPORTS = {
                                                  ctypes.c_void_p, ctypes.c_void_p]),
     "traj_tree_max_nodes": (ctypes.c_int32, [ctypes.POINTER(TreeShape)]),
     "traj_verify_layer_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(AttnShape), ctypes.POINTER(LayerDims)]),
+    "traj_refresh_layer_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(RefreshShape), ctypes.POINTER(LayerDims)]),
+    "traj_refresh_layer": (ctypes.c_int32, [ctypes.c_void_p, ctypes.POINTER(LayerWeights), ctypes.POINTER(LayerDims),
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.POINTER(RefreshShape), ctypes.c_void_p, ctypes.c_size_t,
+                                            ctypes.c_void_p]),
     "traj_verify_layer": (ctypes.c_int32, [ctypes.c_void_p, ctypes.POINTER(LayerWeights), ctypes.POINTER(LayerDims),
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                            ctypes.POINTER(AttnShape), ctypes.c_void_p, ctypes.c_size_t,
@@ -405,6 +416,51 @@ def verify_layer(x, weights, k_cache, v_cache, draft_parent, Hq, pos0=None, inte
                                   workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "traj_verify_layer")
     return x
+
+
+def refresh_layer_workspace_size(B, S, L, Hq, Hkv, D, hidden, inter, rms_eps=1e-5, rope_theta=500000.0):
+    sh = RefreshShape(B, S, L, Hq, Hkv, D, 0.0)
+    return int(_lib().traj_refresh_layer_workspace_size(ctypes.byref(sh),
+                                                        ctypes.byref(LayerDims(hidden, inter, rms_eps, rope_theta))))
+
+
+def refresh_layer(x, weights, block_start, Hq, Hkv, L, k_cache=None, v_cache=None, inter=None, rms_eps=1e-5,
+                  rope_theta=500000.0, scale=0.0, workspace=None, stream=None):
+    """Dual-cache refresh: one decoder layer over whole sequences x [B, S + L, hidden] (bf16,
+    updated in place) with bidirectional attention; the rotated K and the V of every position
+    outside each sequence's block [block_start[b], block_start[b] + L) go to k_cache / v_cache
+    [B, S, Hkv, D] (allocated when None).  Returns (x, k_cache, v_cache)."""
+    B, T, hidden = x.shape
+    S = T - L
+    D = hidden // Hq
+    if inter is None:
+        inter = weights["w_down"].shape[0]
+    _dev(x, "x", torch.bfloat16)
+    for n in LAYER_WEIGHTS:
+        _dev(weights[n], n, torch.bfloat16)
+    for n, shape in (("attn_norm", (hidden,)), ("w_qkv", (hidden, (Hq + 2 * Hkv) * D)), ("w_o", (Hq * D, hidden)),
+                     ("mlp_norm", (hidden,)), ("w_gate_up", (hidden, 2 * inter)), ("w_down", (inter, hidden))):
+        _expect_shape(weights[n], n, shape)
+    _dev(block_start, "block_start", torch.int32)
+    _expect_shape(block_start, "block_start", (B,))
+    if k_cache is None:
+        k_cache = torch.empty(B, S, Hkv, D, dtype=torch.bfloat16, device=x.device)
+    if v_cache is None:
+        v_cache = torch.empty(B, S, Hkv, D, dtype=torch.bfloat16, device=x.device)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, n, torch.bfloat16)
+        _expect_shape(t, n, (B, S, Hkv, D))
+    sh = RefreshShape(B, S, L, Hq, Hkv, D, float(scale))
+    dims = LayerDims(hidden, inter, rms_eps, rope_theta)
+    need = int(_lib().traj_refresh_layer_workspace_size(ctypes.byref(sh), ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+    lw = LayerWeights(*[weights[n].data_ptr() for n in LAYER_WEIGHTS])
+    st = _lib().traj_refresh_layer(_ptr(x), ctypes.byref(lw), ctypes.byref(dims), _ptr(block_start), _ptr(k_cache),
+                                   _ptr(v_cache), ctypes.byref(sh), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "traj_refresh_layer")
+    return x, k_cache, v_cache
 
 
 def linear_workspace_size(M, K, N):

@@ -8,6 +8,8 @@
 //                      sits at position pos0[b] + p (the drafts are alternative states of the
 //                      same block)
 //   swiglu_kernel      act = silu(gate) * up from the [gate | up] rows of the gate/up projection
+//   cache_gather_kernel  the dual-cache refresh's copy of the rotated K / V rows outside the
+//                      current block into the prefix | suffix cache
 #pragma once
 
 #include "common.hpp"
@@ -115,23 +117,59 @@ __global__ __launch_bounds__(kLayerThreads) void rope_split_kernel(const uint16_
         *reinterpret_cast<u32x4_t*>(vdst + 8 * i) = *reinterpret_cast<const u32x4_t*>(vsrc + 8 * i);
 }
 
-// gu: [T, 2 I] rows [gate | up]; act: [T, I].  grid (ceil(I / (8 * threads)), T); I % 8 == 0.
+// gu: [T, 2 I] rows [gate | up]; act: [T, I].  Grid-stride over the T * I / 8 chunks of
+// 8 elements (I % 8 == 0).
 __global__ __launch_bounds__(kLayerThreads) void swiglu_kernel(const uint16_t* __restrict__ gu,
-                                                               uint16_t* __restrict__ act, int I) {
-    const int t = blockIdx.y;
-    const int i = blockIdx.x * kLayerThreads + threadIdx.x;  // 8-element chunk
-    if (i >= I / 8) return;
-    const u32x4_t g = *reinterpret_cast<const u32x4_t*>(gu + (int64_t)t * 2 * I + 8 * i);
-    const u32x4_t u = *reinterpret_cast<const u32x4_t*>(gu + (int64_t)t * 2 * I + I + 8 * i);
-    u32x4_t o;
+                                                               uint16_t* __restrict__ act, int64_t T, int I) {
+    const int cpr = I / 8;  // chunks per row
+    const int64_t total = T * cpr;
+    for (int64_t q = (int64_t)blockIdx.x * kLayerThreads + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * kLayerThreads) {
+        const int64_t t = q / cpr;
+        const int i = (int)(q - t * cpr);
+        const u32x4_t g = *reinterpret_cast<const u32x4_t*>(gu + t * 2 * I + 8 * i);
+        const u32x4_t u = *reinterpret_cast<const u32x4_t*>(gu + t * 2 * I + I + 8 * i);
+        u32x4_t o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const float g0 = bf16_lo(g[e]), g1 = bf16_hi(g[e]);
-        const float a = g0 / (1.0f + __expf(-g0)) * bf16_lo(u[e]);
-        const float c = g1 / (1.0f + __expf(-g1)) * bf16_hi(u[e]);
-        o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(c) << 16);
+        for (int e = 0; e < 4; ++e) {
+            const float g0 = bf16_lo(g[e]), g1 = bf16_hi(g[e]);
+            const float a = g0 / (1.0f + __expf(-g0)) * bf16_lo(u[e]);
+            const float c = g1 / (1.0f + __expf(-g1)) * bf16_hi(u[e]);
+            o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(c) << 16);
+        }
+        *reinterpret_cast<u32x4_t*>(act + t * I + 8 * i) = o;
     }
-    *reinterpret_cast<u32x4_t*>(act + (int64_t)t * I + 8 * i) = o;
+}
+
+// Dual-cache refresh: the rotated K and V rows of every position outside the current block go
+// to the cache, prefix rows then suffix rows.  kd / vd: [B, T, Hkv D] (T = S + L positions);
+// caches: [B, S, Hkv D]; block_start[b] in [0, S] (a value outside is reported and clamped).
+// Grid-stride over the B * S * Hkv D / 8 chunks of 8 elements.
+__global__ __launch_bounds__(kLayerThreads) void cache_gather_kernel(const uint16_t* __restrict__ kd,
+                                                                     const uint16_t* __restrict__ vd,
+                                                                     const int32_t* __restrict__ block_start,
+                                                                     uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+                                                                     int B, int S, int L, int width) {
+    const int cpr = width / 8;  // chunks per key row
+    const int64_t total = (int64_t)B * S * cpr;
+    const int T = S + L;
+    for (int64_t q = (int64_t)blockIdx.x * kLayerThreads + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * kLayerThreads) {
+        const int64_t row = q / cpr;  // b S + s
+        const int c = (int)(q - row * cpr);
+        const int b = (int)(row / S);
+        const int sp = (int)(row - (int64_t)b * S);
+        int bs = block_start[b];
+        if (bs < 0 || bs > S) {
+            if (sp == 0 && c == 0) flag_device_status(4);
+            bs = bs < 0 ? 0 : S;
+        }
+        const int t = sp < bs ? sp : sp + L;  // position in the sequence
+        const int64_t src = ((int64_t)b * T + t) * width + 8 * c;
+        const int64_t dst = row * width + 8 * c;
+        *reinterpret_cast<u32x4_t*>(kc + dst) = *reinterpret_cast<const u32x4_t*>(kd + src);
+        *reinterpret_cast<u32x4_t*>(vc + dst) = *reinterpret_cast<const u32x4_t*>(vd + src);
+    }
 }
 
 }  // namespace trajspec

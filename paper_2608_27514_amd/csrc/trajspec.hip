@@ -218,6 +218,103 @@ traj_status check_layer(const traj_attn_shape* sh, const traj_layer_dims* dm) {
     return TRAJ_OK;
 }
 
+traj_status check_weights(const void* x, const traj_layer_weights* w) {
+    if (w == nullptr || w->attn_norm == nullptr || w->w_qkv == nullptr || w->w_o == nullptr ||
+        w->mlp_norm == nullptr || w->w_gate_up == nullptr || w->w_down == nullptr)
+        return TRAJ_E_NULL;
+    if (!aligned16(x) || !aligned16(w->attn_norm) || !aligned16(w->mlp_norm) || !aligned16(w->w_qkv) ||
+        !aligned16(w->w_o) || !aligned16(w->w_gate_up) || !aligned16(w->w_down))
+        return TRAJ_E_SHAPE;
+    return TRAJ_OK;
+}
+
+// The refresh's layer runs over B whole sequences of T = S + L tokens; `as` receives the
+// equivalent attention shape (one "draft" of T tokens, the sequence's own K / V as its cache).
+traj_status check_refresh(const traj_refresh_shape* sh, const traj_layer_dims* dm, traj_attn_shape* as) {
+    if (sh == nullptr || dm == nullptr) return TRAJ_E_NULL;
+    if (sh->B < 1 || sh->S < 0 || sh->L < 1 || (int64_t)sh->S + sh->L > 0x7fffffff / 2) return TRAJ_E_SHAPE;
+    *as = traj_attn_shape{sh->B, 1, sh->S + sh->L, sh->Hq, sh->Hkv, sh->D, sh->S + sh->L, sh->scale};
+    return check_layer(as, dm);
+}
+
+// Cache-only attention: every query row of q [B, T, Hq, D] attends to the S keys of k / v
+// [B, S, Hkv, D] (the attention kernel with empty draft visible sets, N = 1, L = T).
+traj_status attn_cache_only(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* out, int B, int T,
+                            int S, int Hq, int Hkv, int D, float scale_in, hipStream_t s) {
+    const traj_attn_shape sh{B, 1, T, Hq, Hkv, D, S, scale_in};
+    const traj_status st = check_attn(&sh);
+    if (st != TRAJ_OK) return st;
+    AttnParams p{};
+    p.q = q;
+    p.kc = k;
+    p.vc = v;
+    p.kd = k;  // never read: no draft is visible
+    p.vd = v;
+    p.parent = nullptr;
+    p.peers = nullptr;
+    p.out = out;
+    p.B = B;
+    p.N = 1;
+    p.L = T;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.S = S;
+    p.group = Hq / Hkv;
+    p.rows_per_group = p.group * T;
+    const int rb = (p.rows_per_group + 31) / 32;
+    p.wg_per_group = (rb + kAttnWaves - 1) / kAttnWaves;
+    const int64_t nwg = (int64_t)B * Hkv * p.wg_per_group;
+    if (nwg > 0x7fffffff) return TRAJ_E_SHAPE;
+    p.num_wg = (int)nwg;
+    const float scale = scale_in > 0.f ? scale_in : 1.0f / std::sqrt((float)D);
+    p.scale_log2 = scale * 1.4426950408889634f;
+    p.drafts_visible = 0;
+    return D == 128 ? launch_attn<128>(p, s) : launch_attn<64>(p, s);
+}
+
+// One pre-norm decoder layer over T packed tokens (x [T, hidden], updated in place).  The rotary
+// position of token t is pos0[t / rope_nl] + t % rope_l (pos0 may be null = 0); `attend` runs
+// between the rotary split and the O projection: it reads the q / k / v rows and writes the
+// attention output a [T, Hq D].
+template <typename Attend>
+traj_status run_layer(uint16_t* xs, const traj_layer_weights* w, const traj_layer_dims* dims, int64_t T, int Hq,
+                      int Hkv, int D, const int32_t* pos0, int rope_nl, int rope_l, const LayerPlan& plan, char* ws,
+                      hipStream_t s, Attend attend) {
+    auto buf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
+    const int hidden = dims->hidden, inter = dims->inter;
+    const int qkv_w = (Hq + 2 * Hkv) * D;
+    void* split = ws + plan.split;
+    const size_t split_bytes = plan.split_bytes;
+    traj_status st;
+    // attention block
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
+                       static_cast<const uint16_t*>(w->attn_norm), buf(plan.xn), hidden, dims->rms_eps);
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false, split,
+                   split_bytes, s)) != TRAJ_OK)
+        return st;
+    hipLaunchKernelGGL(rope_split_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, buf(plan.qkv), pos0,
+                       buf(plan.q), buf(plan.kd), buf(plan.vd), rope_nl, rope_l, Hq, Hkv, D,
+                       std::log2(dims->rope_theta));
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = attend(buf(plan.q), buf(plan.kd), buf(plan.vd), buf(plan.a))) != TRAJ_OK) return st;
+    if ((st = gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, (int64_t)Hq * D, true, split,
+                   split_bytes, s)) != TRAJ_OK)
+        return st;
+    // MLP block
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
+                       static_cast<const uint16_t*>(w->mlp_norm), buf(plan.xn), hidden, dims->rms_eps);
+    if ((st = launched()) != TRAJ_OK) return st;
+    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter, hidden,
+                   false, split, split_bytes, s)) != TRAJ_OK)
+        return st;
+    const int64_t chunks = T * (inter / 8);
+    hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)std::min<int64_t>((chunks + kLayerThreads - 1) / kLayerThreads, 16384)),
+                       dim3(kLayerThreads), 0, s, buf(plan.gu), buf(plan.act), T, inter);
+    if ((st = launched()) != TRAJ_OK) return st;
+    return gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, split, split_bytes, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -274,6 +371,7 @@ traj_status traj_verify_attn_peers(const void* q, const void* k_cache, const voi
     p.num_wg = (int)nwg;
     const float scale = shape->scale > 0.f ? shape->scale : 1.0f / std::sqrt((float)shape->D);
     p.scale_log2 = scale * 1.4426950408889634f;
+    p.drafts_visible = 1;
     hipStream_t s = as_stream(stream);
     return shape->D == 128 ? launch_attn<128>(p, s) : launch_attn<64>(p, s);
 }
@@ -420,53 +518,59 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* w, const traj_l
                               const traj_attn_shape* shape, void* workspace, size_t workspace_bytes, void* stream) {
     traj_status st = check_layer(shape, dims);
     if (st != TRAJ_OK) return st;
-    if (x == nullptr || w == nullptr || draft_parent == nullptr || workspace == nullptr) return TRAJ_E_NULL;
-    if (w->attn_norm == nullptr || w->w_qkv == nullptr || w->w_o == nullptr || w->mlp_norm == nullptr ||
-        w->w_gate_up == nullptr || w->w_down == nullptr)
-        return TRAJ_E_NULL;
+    if (x == nullptr || draft_parent == nullptr || workspace == nullptr) return TRAJ_E_NULL;
+    if ((st = check_weights(x, w)) != TRAJ_OK) return st;
     if (shape->S > 0 && (k_cache == nullptr || v_cache == nullptr)) return TRAJ_E_NULL;
-    if (!aligned16(x) || !aligned16(w->attn_norm) || !aligned16(w->mlp_norm) || !aligned16(w->w_qkv) ||
-        !aligned16(w->w_o) || !aligned16(w->w_gate_up) || !aligned16(w->w_down))
-        return TRAJ_E_SHAPE;
     const LayerPlan plan = plan_layer(shape, dims);
     if (workspace_bytes < plan.total || reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return TRAJ_E_WORKSPACE;
-    char* ws = static_cast<char*>(workspace);
-    auto buf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
-    hipStream_t s = as_stream(stream);
     const int64_t T = (int64_t)shape->B * shape->N * shape->L;
-    const int hidden = dims->hidden, inter = dims->inter;
-    const int qkv_w = (shape->Hq + 2 * shape->Hkv) * shape->D;
-    uint16_t* xs = static_cast<uint16_t*>(x);
-    // attention block
-    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
-                       static_cast<const uint16_t*>(w->attn_norm), buf(plan.xn), hidden, dims->rms_eps);
-    if ((st = launched()) != TRAJ_OK) return st;
-    void* split = ws + plan.split;
-    const size_t split_bytes = plan.split_bytes;
-    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_qkv), buf(plan.qkv), T, qkv_w, hidden, false, split,
-                   split_bytes, s)) != TRAJ_OK)
-        return st;
-    hipLaunchKernelGGL(rope_split_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, buf(plan.qkv), pos0,
-                       buf(plan.q), buf(plan.kd), buf(plan.vd), shape->N * shape->L, shape->L, shape->Hq, shape->Hkv,
-                       shape->D, std::log2(dims->rope_theta));
-    if ((st = launched()) != TRAJ_OK) return st;
-    if ((st = traj_verify_attn(buf(plan.q), k_cache, v_cache, buf(plan.kd), buf(plan.vd), draft_parent, buf(plan.a),
-                               shape, nullptr, 0, stream)) != TRAJ_OK)
-        return st;
-    if ((st = gemm(buf(plan.a), static_cast<const uint16_t*>(w->w_o), xs, T, hidden, shape->Hq * shape->D, true, split,
-                   split_bytes, s)) != TRAJ_OK)
-        return st;
-    // MLP block
-    hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)T), dim3(kLayerThreads), 0, s, xs,
-                       static_cast<const uint16_t*>(w->mlp_norm), buf(plan.xn), hidden, dims->rms_eps);
-    if ((st = launched()) != TRAJ_OK) return st;
-    if ((st = gemm(buf(plan.xn), static_cast<const uint16_t*>(w->w_gate_up), buf(plan.gu), T, 2 * (int64_t)inter, hidden,
-                   false, split, split_bytes, s)) != TRAJ_OK)
-        return st;
-    hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((inter / 8 + kLayerThreads - 1) / kLayerThreads), (unsigned)T),
-                       dim3(kLayerThreads), 0, s, buf(plan.gu), buf(plan.act), inter);
-    if ((st = launched()) != TRAJ_OK) return st;
-    return gemm(buf(plan.act), static_cast<const uint16_t*>(w->w_down), xs, T, hidden, inter, true, split, split_bytes, s);
+    // every draft's token p sits at position pos0[b] + p
+    return run_layer(static_cast<uint16_t*>(x), w, dims, T, shape->Hq, shape->Hkv, shape->D, pos0,
+                     shape->N * shape->L, shape->L, plan, static_cast<char*>(workspace), as_stream(stream),
+                     [&](const uint16_t* q, const uint16_t* kd, const uint16_t* vd, uint16_t* a) {
+                         return traj_verify_attn(q, k_cache, v_cache, kd, vd, draft_parent, a, shape, nullptr, 0, stream);
+                     });
+}
+
+size_t traj_refresh_layer_workspace_size(const traj_refresh_shape* shape, const traj_layer_dims* dims) {
+    traj_attn_shape as{};
+    if (check_refresh(shape, dims, &as) != TRAJ_OK) return 0;
+    return plan_layer(&as, dims).total;
+}
+
+traj_status traj_refresh_layer(void* x, const traj_layer_weights* w, const traj_layer_dims* dims,
+                               const int32_t* block_start, void* k_cache, void* v_cache,
+                               const traj_refresh_shape* shape, void* workspace, size_t workspace_bytes, void* stream) {
+    traj_attn_shape as{};
+    traj_status st = check_refresh(shape, dims, &as);
+    if (st != TRAJ_OK) return st;
+    if (x == nullptr || block_start == nullptr || workspace == nullptr) return TRAJ_E_NULL;
+    if ((st = check_weights(x, w)) != TRAJ_OK) return st;
+    if (shape->S > 0 && (k_cache == nullptr || v_cache == nullptr)) return TRAJ_E_NULL;
+    if (shape->S > 0 && (!aligned16(k_cache) || !aligned16(v_cache))) return TRAJ_E_SHAPE;
+    const LayerPlan plan = plan_layer(&as, dims);
+    if (workspace_bytes < plan.total || reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return TRAJ_E_WORKSPACE;
+    const int Tseq = shape->S + shape->L;
+    const int64_t T = (int64_t)shape->B * Tseq;
+    hipStream_t s = as_stream(stream);
+    // positions 0 .. T - 1 of each sequence; attention over the sequence's own K / V (the
+    // kernel's cache-only mode), after the rows outside the block have been copied to the cache
+    return run_layer(static_cast<uint16_t*>(x), w, dims, T, shape->Hq, shape->Hkv, shape->D, nullptr, Tseq, Tseq,
+                     plan, static_cast<char*>(workspace), s,
+                     [&](const uint16_t* q, const uint16_t* kd, const uint16_t* vd, uint16_t* a) -> traj_status {
+                         if (shape->S > 0) {
+                             const int width = shape->Hkv * shape->D;
+                             const int64_t chunks = (int64_t)shape->B * shape->S * (width / 8);
+                             const unsigned grid = (unsigned)std::min<int64_t>((chunks + kLayerThreads - 1) / kLayerThreads, 8192);
+                             hipLaunchKernelGGL(cache_gather_kernel, dim3(grid), dim3(kLayerThreads), 0, s, kd, vd,
+                                                block_start, static_cast<uint16_t*>(k_cache),
+                                                static_cast<uint16_t*>(v_cache), shape->B, shape->S, shape->L, width);
+                             const traj_status gs = launched();
+                             if (gs != TRAJ_OK) return gs;
+                         }
+                         return attn_cache_only(q, kd, vd, a, shape->B, Tseq, Tseq, shape->Hq, shape->Hkv, shape->D,
+                                                shape->scale, s);
+                     });
 }
 
 size_t traj_linear_workspace_size(int64_t M, int64_t K, int64_t N) { return gemm_workspace_bytes(M, N, K); }

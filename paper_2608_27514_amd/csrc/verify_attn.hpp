@@ -44,6 +44,10 @@
 //      per-draft peer masks add drafts to a draft's visible set (inter-block speculation).
 //      Tiles that hold only fully visible blocks need no per-element mask (always the case
 //      when L is a multiple of 32 and a wave's rows share a draft).
+//   With drafts_visible = 0 every visible set is empty and phase 2 does nothing: the queries
+//   attend to the S cache keys only.  The dual-cache refresh uses this for bidirectional
+//   attention over whole sequences (its "cache" is the sequence's own K / V, N = 1 and L = the
+//   sequence length, no parent array).
 #pragma once
 
 #include "common.hpp"
@@ -65,6 +69,7 @@ struct AttnParams {
     int wg_per_group;    // workgroups per (b, g)
     int num_wg;
     float scale_log2;    // softmax scale * log2(e)
+    int drafts_visible;  // 1: each draft sees its root path (+ peers); 0: queries see the cache only
 };
 
 constexpr int kAttnWaves = 4;
@@ -428,7 +433,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
 
     // The parent array (ancestor walk below) is loaded first: the walk then waits for this
     // load only, not for the Q, K and stage loads issued after it.
-    const int pj = (wave == 0 && lane < N) ? P.parent[(int64_t)b * N + lane] : -1;
+    const int pj = (P.parent != nullptr && wave == 0 && lane < N) ? P.parent[(int64_t)b * N + lane] : -1;
     const uint64_t peer_bits = (P.peers != nullptr && wave == 0 && lane < N) ? P.peers[(int64_t)b * N + lane] : 0ull;
 
     // This lane's query row (lanes l and l^32 share a row).
@@ -541,7 +546,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
         // drafts made visible beyond the root path (the joint trees of inter-block
         // speculation), restricted to the N drafts of the sequence
         const uint64_t in_range = N == 64 ? ~0ull : ((1ull << N) - 1ull);
-        if (lane < N) anc[lane] = msk | (peer_bits & in_range);
+        if (lane < N) anc[lane] = P.drafts_visible ? (msk | (peer_bits & in_range)) : 0ull;
     }
     if (nb > 0) {
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);

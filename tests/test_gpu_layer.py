@@ -162,3 +162,71 @@ def test_linear_rejects_bad_shapes():
         tsp.linear(x, torch.zeros(60, 64, dtype=torch.bfloat16, device="cuda"))
     with pytest.raises(ValueError):
         tsp.linear(x, torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda"))
+
+
+# ---------------------------------------------------------------- dual-cache refresh (App. A)
+
+@pytest.mark.parametrize("B,S,L,Hq,Hkv,D,inter,starts", [
+    (2, 40, 8, 2, 2, 128, 512, [0, 40]),          # block first / last
+    (1, 70, 5, 4, 2, 64, 384, [33]),              # GQA, D 64, ragged lengths
+    (2, 100, 32, 8, 4, 128, 3072, [64, 0]),       # few rows: split-K projections
+])
+def test_refresh_layer_parity(B, S, L, Hq, Hkv, D, inter, starts):
+    rng = np.random.default_rng(S * 10 + L)
+    hidden = Hq * D
+    x = bf16_round(rng.standard_normal((B, S + L, hidden)))
+    w = _weights(rng, hidden, Hq, Hkv, D, inter)
+    ref, ref_k, ref_v = oracle.refresh_layer(x, w, starts, L, Hq, Hkv)
+    bf = lambda a: cuda(np.asarray(a, dtype=np.float32), torch.bfloat16)  # noqa: E731
+    xg = bf(x)
+    out, kc, vc = tsp.refresh_layer(xg, {k: bf(v) for k, v in w.items()}, cuda(np.array(starts), torch.int32),
+                                    Hq, Hkv, L)
+    torch.cuda.synchronize()
+    assert out.data_ptr() == xg.data_ptr()
+    for got, want in ((out, ref), (kc, ref_k), (vc, ref_v)):
+        g = got.float().cpu().numpy().astype(np.float64)
+        err = np.abs(g - want)
+        rms = math.sqrt(float(np.mean(want * want)))
+        assert (err <= 0.03 * np.abs(want) + 0.03 * rms).all(), float((err - 0.03 * np.abs(want) - 0.03 * rms).max())
+        assert float(err.mean()) < 2e-3 * rms
+
+
+def test_refresh_then_verify_root_state_agrees():
+    """Refresh a sequence's cache at a block boundary, then verify the block's current state as
+    the only draft against that cache: the verification layer's output equals the refresh
+    layer's output for the block rows (same visible keys and positions, different kernels)."""
+    rng = np.random.default_rng(77)
+    B, S, L, Hq, Hkv, D, inter = 2, 96, 32, 4, 2, 128, 1024
+    hidden = Hq * D
+    x = bf16_round(rng.standard_normal((B, S + L, hidden)))
+    w = {k: cuda(np.asarray(v, dtype=np.float32), torch.bfloat16)
+         for k, v in _weights(rng, hidden, Hq, Hkv, D, inter).items()}
+    starts = np.array([32, 96], dtype=np.int32)
+    xg = cuda(np.asarray(x, dtype=np.float32), torch.bfloat16)
+    blocks = torch.stack([xg[b, starts[b]:starts[b] + L] for b in range(B)])[:, None].contiguous()  # [B,1,L,h]
+    out, kc, vc = tsp.refresh_layer(xg, w, cuda(starts, torch.int32), Hq, Hkv, L)
+    ver = tsp.verify_layer(blocks, w, kc, vc, cuda(np.full((B, 1), -1), torch.int32), Hq,
+                           pos0=cuda(starts, torch.int32))
+    torch.cuda.synchronize()
+    # both sides round every stored activation to bf16 but accumulate in different orders
+    # (one pass over all keys against cache-then-block; different GEMM tilings), so they agree
+    # to the layer's compounded rounding: the bound of the layer parity test
+    for b in range(B):
+        a = ver[b, 0].float().cpu().numpy().astype(np.float64)
+        r = out[b, starts[b]:starts[b] + L].float().cpu().numpy().astype(np.float64)
+        err = np.abs(a - r)
+        rms = math.sqrt(float(np.mean(r * r)))
+        assert (err <= 0.03 * np.abs(r) + 0.03 * rms).all()
+        assert float(err.mean()) < 2e-3 * rms
+
+
+def test_refresh_reports_a_block_outside_the_sequence():
+    rng = np.random.default_rng(5)
+    B, S, L, Hq, Hkv, D, inter = 2, 16, 4, 1, 1, 64, 128
+    x = cuda(np.asarray(bf16_round(rng.standard_normal((B, S + L, Hq * D))), dtype=np.float32), torch.bfloat16)
+    w = {k: cuda(np.asarray(v, dtype=np.float32), torch.bfloat16)
+         for k, v in _weights(rng, Hq * D, Hq, Hkv, D, inter).items()}
+    tsp.device_status(reset=True)
+    _, kc, _ = tsp.refresh_layer(x, w, cuda(np.array([3, 99]), torch.int32), Hq, Hkv, L)
+    assert tsp.device_status(reset=True) & tsp.DEV_BAD_BLOCK
+    assert torch.isfinite(kc.float()).all()

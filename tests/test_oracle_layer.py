@@ -1,6 +1,8 @@
 """Pins of the verification-layer oracle: bf16 rounding against torch, RMSNorm and rotary
 closed forms and invariants, SwiGLU against torch, the residual identity, and the whole layer
-against the nested-loop re-derivation (CPU only)."""
+against the nested-loop re-derivation; of the refresh layer: full attention against torch's
+SDPA, the cache's dependence on its own positions only, and agreement with the verification
+layer for the block's root state (CPU only)."""
 
 import math
 
@@ -9,7 +11,7 @@ import pytest
 import torch
 
 from oracle.brute import layer_scalar
-from oracle.layer import bf16_round, linear, rmsnorm, rope, silu, verify_layer
+from oracle.layer import bf16_round, full_attention, linear, refresh_layer, rmsnorm, rope, silu, verify_layer
 
 
 def test_bf16_round_matches_torch():
@@ -95,3 +97,69 @@ def test_layer_against_scalar_loops(seed):
     frac_equal = float(np.mean(a == b))
     assert frac_equal > 0.95, frac_equal
     assert np.allclose(a, b, rtol=2e-2, atol=2e-2)
+
+
+def test_full_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(20)
+    T, Hq, Hkv, D = 11, 4, 2, 16
+    q, k, v = rng.standard_normal((T, Hq, D)), rng.standard_normal((T, Hkv, D)), rng.standard_normal((T, Hkv, D))
+    got = full_attention(q, k, v, scale=0.3)
+    tq = torch.tensor(q).permute(1, 0, 2)
+    tk = torch.tensor(np.repeat(k, 2, axis=1)).permute(1, 0, 2)
+    tv = torch.tensor(np.repeat(v, 2, axis=1)).permute(1, 0, 2)
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=0.3).permute(1, 0, 2).numpy()
+    assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def _refresh_case(seed, B=1, S=9, L=4, Hq=2, Hkv=1, D=8, inter=16):
+    rng = np.random.default_rng(seed)
+    x = bf16_round(rng.standard_normal((B, S + L, Hq * D)))
+    return rng, x, _weights(rng, Hq * D, Hq, Hkv, D, inter)
+
+
+def test_refresh_cache_depends_on_its_own_positions_only():
+    rng, x, w = _refresh_case(21)
+    L, Hq, Hkv = 4, 2, 1
+    _, kc, vc = refresh_layer(x, w, [3], L, Hq, Hkv)
+    # the block's own rows do not reach the cache
+    x2 = x.copy()
+    x2[0, 3:7] = bf16_round(rng.standard_normal((4, x.shape[2])))
+    _, kc2, vc2 = refresh_layer(x2, w, [3], L, Hq, Hkv)
+    assert np.array_equal(kc, kc2) and np.array_equal(vc, vc2)
+    # a prefix row changes its own cache row only; the suffix starts after the block
+    x3 = x.copy()
+    x3[0, 1] = bf16_round(rng.standard_normal(x.shape[2]))
+    _, kc3, vc3 = refresh_layer(x3, w, [3], L, Hq, Hkv)
+    changed = np.any(kc3 != kc, axis=(0, 2, 3)) | np.any(vc3 != vc, axis=(0, 2, 3))
+    assert changed.tolist() == [s == 1 for s in range(9)]
+    x4 = x.copy()
+    x4[0, 10] = bf16_round(rng.standard_normal(x.shape[2]))  # position 10 = cache row 6
+    _, kc4, _ = refresh_layer(x4, w, [3], L, Hq, Hkv)
+    assert np.any(kc4 != kc, axis=(0, 2, 3)).tolist() == [s == 6 for s in range(9)]
+
+
+def test_refresh_positions_rotate_identical_rows():
+    """Identical token rows at every position: V rows are identical, K rows are rotations of one
+    vector (same norm per head, different values), so the positions are applied."""
+    rng, x, w = _refresh_case(22)
+    x[0, :] = x[0, 0]
+    _, kc, vc = refresh_layer(x, w, [0], 4, 2, 1)
+    assert np.all(vc == vc[:, :1])
+    norms = np.linalg.norm(kc, axis=-1)
+    assert np.allclose(norms, norms[:, :1], rtol=2e-2)
+    assert len({kc[0, s].tobytes() for s in range(kc.shape[1])}) == kc.shape[1]
+
+
+def test_refresh_then_verify_root_state_agrees():
+    """The dual cache's contract: verifying the block's current state (one draft, no parent)
+    against the refreshed cache, at positions block_start + p, gives the refresh layer's own
+    output for the block rows -- two different attention paths over the same visible keys."""
+    rng, x, w = _refresh_case(23, B=2, S=10, L=5, Hq=2, Hkv=2, D=8, inter=16)
+    bs = [4, 10]
+    out, kc, vc = refresh_layer(x, w, bs, 5, 2, 2)
+    for b in range(2):
+        xb = x[b:b + 1, bs[b]:bs[b] + 5][:, None]  # [1, 1, L, hidden]
+        ver = verify_layer(xb, w, kc[b:b + 1], vc[b:b + 1], np.array([[-1]]), 2, pos0=np.array([bs[b]]))
+        ref = out[b, bs[b]:bs[b] + 5]
+        assert np.allclose(ver[0, 0], ref, rtol=2 ** -7, atol=2 ** -7 * np.abs(ref).max())
+        assert np.mean(ver[0, 0] == ref) > 0.95
