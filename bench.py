@@ -318,6 +318,52 @@ def time_layer_one_sequence(wl, stream, reps=20):
                        seed_for(wl.cid, salt=41), stream, reps)
 
 
+def time_refresh(wl, stream, reps=3):
+    """The dual-cache refresh at a block boundary (traj_refresh_layer: one decoder layer over
+    whole sequences, bidirectional attention, prefix / suffix K and V written to the cache), for
+    one sequence (prefix 512, block 32, suffix 224) and for the workload's batch (its prefix,
+    block and suffix), random-init weights of the 8B layer shape."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed_for(wl.cid, salt=43))
+    hidden, inter = wl.Hq * wl.D, 3 * wl.Hq * wl.D
+    qkv = (wl.Hq + 2 * wl.Hkv) * wl.D
+
+    def r(*shape, scale=1.0):
+        return (torch.randn(*shape, device=dev, generator=g) * scale).to(torch.bfloat16)
+
+    w = {"attn_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16), "w_qkv": r(hidden, qkv, scale=hidden ** -0.5),
+         "w_o": r(wl.Hq * wl.D, hidden, scale=hidden ** -0.5),
+         "mlp_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16),
+         "w_gate_up": r(hidden, 2 * inter, scale=hidden ** -0.5), "w_down": r(inter, hidden, scale=inter ** -0.5)}
+    out = {}
+    for name, B, prefix, suffix in (("one_sequence", 1, 512, 224), ("batch", wl.B, wl.S_prefix, wl.S_suffix)):
+        S, L = prefix + suffix, wl.L
+        x0 = r(B, S + L, hidden)
+        x = x0.clone()
+        starts = torch.full((B,), prefix, dtype=torch.int32, device=dev)
+        kc = torch.empty(B, S, wl.Hkv, wl.D, dtype=torch.bfloat16, device=dev)
+        vc = torch.empty_like(kc)
+        ws = torch.empty(tsp.refresh_layer_workspace_size(B, S, L, wl.Hq, wl.Hkv, wl.D, hidden, inter),
+                         dtype=torch.uint8, device=dev)
+        total = 0.0
+        for i in range(reps + 1):  # the first call warms up
+            x.copy_(x0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            tsp.refresh_layer(x, w, starts, wl.Hq, wl.Hkv, L, k_cache=kc, v_cache=vc, workspace=ws, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if i > 0:
+                total += e0.elapsed_time(e1)
+        T = B * (S + L)
+        out[name] = {"sequences": B, "tokens": T, "cache_rows": S, "ms_per_layer": total / reps,
+                     "gemm_tflop": 2.0 * T * hidden * (qkv + hidden + 3 * inter) / 1e12,
+                     "attention_tflop": 4.0 * B * (S + L) ** 2 * wl.D * wl.Hq / 1e12}
+        del x0, x, kc, vc, ws
+    return out
+
+
 def _time_layer(B, N, L, Hq, Hkv, D, S, S_prefix, kc, vc, parent, seed, stream, reps):
     dev = kc.device
     hidden, inter = Hq * D, 3 * Hq * D
@@ -456,6 +502,7 @@ def main():
     tree = None if args.no_extras else time_tree_build(x, buf, tau, stream)
     layer = None if args.no_extras else time_layer(x, stream)
     layer_one = None if args.no_extras else time_layer_one_sequence(wl, stream)
+    refresh = None if args.no_extras else time_refresh(wl, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     status = tsp.device_status(reset=True)
 
@@ -503,6 +550,7 @@ def main():
         "interblock": inter,
         "verify_layer": layer,
         "verify_layer_one_sequence": layer_one,
+        "refresh_layer": refresh,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:
