@@ -404,8 +404,13 @@ __device__ __forceinline__ void full_step(int t, const CacheArgs& a, const AttnL
     bf16x8_t pf[2][2];
     softmax_phase<D>(s, a.c, a.thr, st, o, pf);
     __builtin_amdgcn_sched_barrier(0);
+    // the matrix phase issues at a raised wave priority: when the other wave on the SIMD is in
+    // its softmax phase, the arbiter then keeps the matrix core fed first (-6% on 8b-batched)
+    __builtin_amdgcn_s_setprio(1);
     qk_pair<D>(cur, ln, qf, s);
     pv_pair<D>(cur + G::kTileElems, ln, pf, o);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
 }
