@@ -448,7 +448,7 @@ def main():
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs the verification step on exactly one GPU; "
+        print(json.dumps({"error": "this benchmark runs the verification step on exactly one GPU; "
                                    "sequences shard across GPUs with no exchange, so N>1 is N independent "
                                    "copies of this benchmark and is not launched here"}))
         sys.exit(2)
