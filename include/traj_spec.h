@@ -339,7 +339,7 @@ traj_status traj_verify_layer(void* x, const traj_layer_weights* weights, const 
  * Layouts (bf16): x [B, T, hidden]; k_cache / v_cache [B, S, Hkv, D] (written); block_start [B]
  * int32 device array in [0, S] (a value outside is clamped and sets TRAJ_DEV_BAD_BLOCK).
  * Weights, dims, rounding and limits as traj_verify_layer (shape->scale 0 = 1/sqrt(D)); one
- * sequence's T K / V rows must stay below 2 GiB.
+ * sequence's T K / V rows must stay below 2 GiB.  x, the caches and the workspace must not overlap.
  * workspace: at least traj_refresh_layer_workspace_size() bytes, 256-byte aligned. */
 typedef struct {
     int32_t B, S, L, Hq, Hkv, D;
@@ -365,7 +365,7 @@ traj_status traj_refresh_layer(void* x, const traj_layer_weights* weights, const
  * one or a few sequences' drafts) split K over several workgroups when given at least
  * traj_linear_workspace_size(M, K, N) bytes, 16-byte aligned, for the fp32 partial products
  * (a size of 0 means the shape is never split); with NULL the call runs unsplit.  A non-NULL
- * workspace that is too small or misaligned is TRAJ_E_WORKSPACE.
+ * workspace that is too small or misaligned is TRAJ_E_WORKSPACE; it must not overlap x, w or y.
  * Errors: TRAJ_E_SHAPE (sizes, alignment), TRAJ_E_UNSUPPORTED, TRAJ_E_NULL, TRAJ_E_WORKSPACE,
  * TRAJ_E_HIP (launch). */
 size_t traj_linear_workspace_size(int64_t M, int64_t K, int64_t N);
