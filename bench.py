@@ -364,6 +364,106 @@ def time_refresh(wl, stream, reps=3):
     return out
 
 
+FORWARD_LAYERS = 32  # decoder layers of the 8B models
+
+
+def time_forward_one_sequence(wl, stream, reps=20):
+    """Per-step latency of one sequence's whole verification forward against its number of draft
+    blocks (in kind the per-step latency the paper plots against draft blocks, Sec. 4,
+    computational overhead analysis): 32 verification layers of the 8B
+    shape (random-init weights, one dual cache per layer: prefix 512 + suffix 224), the LM head
+    (traj_linear), the logit pass, acceptance and the next tree (W3D3), captured once as a HIP
+    graph and replayed; the eager time (one Python call per entry point) is given beside it.
+    Drafts 1, 2, 4, 7 are prefixes of the W3D3 hybrid tree.  The final RMSNorm before the LM
+    head is not a library call and is left out (one pass over the draft rows)."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed_for(wl.cid, salt=53))
+    Hq, Hkv, D, L, k, V = wl.Hq, wl.Hkv, wl.D, wl.L, wl.k, wl.V
+    hidden, inter = Hq * D, 3 * Hq * D
+    qkv = (Hq + 2 * Hkv) * D
+    S_prefix, S = 512, 512 + 224
+
+    def r(*shape, scale=1.0):
+        return (torch.randn(*shape, device=dev, generator=g) * scale).to(torch.bfloat16)
+
+    layers = []
+    for _ in range(FORWARD_LAYERS):
+        layers.append({"w": {"attn_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16),
+                             "w_qkv": r(hidden, qkv, scale=hidden ** -0.5), "w_o": r(Hq * D, hidden, scale=hidden ** -0.5),
+                             "mlp_norm": (1 + 0.1 * r(hidden).float()).to(torch.bfloat16),
+                             "w_gate_up": r(hidden, 2 * inter, scale=hidden ** -0.5),
+                             "w_down": r(inter, hidden, scale=inter ** -0.5)},
+                       "kc": r(1, S, Hkv, D), "vc": r(1, S, Hkv, D)})
+    lm_head = r(hidden, V, scale=hidden ** -0.5)
+    pos0 = torch.full((1,), S_prefix, dtype=torch.int32, device=dev)
+    committed = torch.where(torch.rand(1, L, device=dev, generator=g) < 0.75,
+                            torch.full((1, L), -1, dtype=torch.int32, device=dev),
+                            torch.randint(0, V, (1, L), device=dev, generator=g, dtype=torch.int32))
+    conf0 = torch.rand(1, L, k, device=dev, generator=g)
+    idx0 = torch.randint(0, V, (1, L, k), device=dev, generator=g, dtype=torch.int32)
+    out = {"layers": FORWARD_LAYERS, "cache_rows": S, "per_drafts": {}}
+    base = None
+    for n in (1, 2, 4, 7):
+        parent = torch.tensor([W3D3_PARENTS[:n]], dtype=torch.int32, device=dev)
+        tokens = torch.randint(0, V, (1, n, L), device=dev, generator=g, dtype=torch.int32)
+        x0 = r(1, n, L, hidden)
+        x = x0.clone()
+        T = n * L
+        ws = torch.empty(tsp.layer_workspace_size(1, n, L, Hq, Hkv, D, S, hidden, inter), dtype=torch.uint8,
+                         device=dev)
+        logits = torch.empty(T, V, dtype=torch.bfloat16, device=dev)
+        lws = torch.empty(max(tsp.linear_workspace_size(T, hidden, V), 16), dtype=torch.uint8, device=dev)
+        conf = torch.empty(T, k, dtype=torch.float32, device=dev)
+        idx = torch.empty(T, k, dtype=torch.int32, device=dev)
+        cws = torch.empty(max(tsp.confidence_topk_workspace_size(logits, k), 16), dtype=torch.uint8, device=dev)
+        acc = {"leaf": torch.empty(1, dtype=torch.int32, device=dev),
+               "on_path": torch.empty((1, n), dtype=torch.uint8, device=dev),
+               "n_accepted": torch.empty(1, dtype=torch.int32, device=dev),
+               "out_tokens": torch.empty((1, L), dtype=torch.int32, device=dev),
+               "hi": torch.empty((1, n, L), dtype=torch.uint8, device=dev)}
+        acc["leaf"].fill_(-1)  # before the first forward: no accepted draft, the committed state
+        acc["out_tokens"].copy_(committed)
+        targs = (acc["out_tokens"], conf0, idx0, wl.tau, TREE_WIDTH, TREE_DEPTH, k)
+        tkw = dict(leaf=acc["leaf"], conf=conf.view(1, n, L, k), idx=idx.view(1, n, L, k))
+        tkw["out"] = tsp.build_tree(*targs, **tkw)
+
+        def forward(s):
+            x.copy_(x0)
+            for ly in layers:
+                tsp.verify_layer(x, ly["w"], ly["kc"], ly["vc"], parent, Hq, pos0=pos0, workspace=ws, stream=s)
+            tsp.linear(x.view(T, hidden), lm_head, y=logits, workspace=lws, stream=s)
+            tsp.confidence_topk(logits, k, conf=conf, idx=idx, workspace=cws, stream=s)
+            tsp.accept(conf, idx, tokens, parent, committed, conf0, idx0, wl.tau, out=acc, stream=s)
+            tsp.build_tree(*targs, **tkw, stream=s)
+
+        def timed(fn):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            fn()
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+
+        eager_ms = timed(lambda: forward(stream))
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            forward(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        graph_ms = timed(graph.replay)
+        base = graph_ms if base is None else base
+        out["per_drafts"][str(n)] = {"draft_tokens": T, "graph_ms": graph_ms, "eager_ms": eager_ms,
+                                     "vs_one_draft": graph_ms / base}
+        del graph, ws, logits, lws, x, x0
+    del layers, lm_head
+    torch.cuda.empty_cache()
+    return out
+
+
 def _time_layer(B, N, L, Hq, Hkv, D, S, S_prefix, kc, vc, parent, seed, stream, reps):
     dev = kc.device
     hidden, inter = Hq * D, 3 * Hq * D
@@ -504,6 +604,7 @@ def main():
     layer_one = None if args.no_extras else time_layer_one_sequence(wl, stream)
     refresh = None if args.no_extras else time_refresh(wl, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
+    forward = None if args.no_extras else time_forward_one_sequence(wl, stream)
     status = tsp.device_status(reset=True)
 
     result = {
@@ -551,6 +652,7 @@ def main():
         "verify_layer": layer,
         "verify_layer_one_sequence": layer_one,
         "refresh_layer": refresh,
+        "forward_one_sequence": forward,
         "device_status": status,
     }
     if wl.cid == 5 and not args.no_sweep:

@@ -86,6 +86,9 @@ def _linear_bound(a, w, y0, ref):
     (4133, 200, 4104, False), (4133, 136, 4104, True), (4096, 8, 4096, False), (4352, 4160, 3848, True),
     # few tiles: K split over workgroups (fp32 partials in the workspace, then one reduction)
     (300, 2048, 264, True), (130, 1088, 136, True), (224, 3080, 520, False),
+    # one or two drafts' rows (17 .. 64) and up to 255: ragged rows, columns and k, split and not
+    (17, 1000, 264, True), (32, 72, 4104, False), (33, 136, 520, True), (64, 4104, 136, True),
+    (50, 8, 8, False), (129, 4096, 1032, True), (255, 520, 8200, False),
 ])
 def test_linear_parity(M, K, N, acc):
     rng = np.random.default_rng(M * 7 + K + N)
@@ -109,6 +112,10 @@ def test_linear_parity(M, K, N, acc):
     (224, 4096, 126464, False),   # LM head of one sequence's W3D3 drafts
     (224, 12288, 4096, True),     # one sequence's down projection + residual (split K)
     (224, 4096, 4096, True),      # one sequence's O projection + residual (split K)
+    (32, 4096, 12288, False),     # one draft: QKV projection (split K)
+    (32, 12288, 4096, True),      # one draft: down projection + residual (split K)
+    (64, 4096, 24576, False),     # two drafts: gate / up projection
+    (64, 4096, 126464, False),    # two drafts: LM head
 ])
 def test_linear_full_size_sampled_rows(M, K, N, acc):
     """8B-shaped projections in the launch configuration the benchmark times; the oracle checks
