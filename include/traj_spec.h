@@ -32,6 +32,10 @@
  *   - Calls validate their host-visible arguments, enqueue kernels on `stream` (a
  *     hipStream_t passed as void*; NULL = the legacy default stream) and return without
  *     synchronising.  Results are ready when the stream has reached that point.
+ *   - Apart from traj_get_device_status, a call enqueues kernel launches only (no memory
+ *     set, copy, allocation or synchronisation), so a sequence of calls on a stream being
+ *     captured into a HIP graph can be replayed; every reduction runs in a fixed order, so
+ *     a replay gives the same bits as the eager calls on the same inputs.
  *   - Errors are returned as traj_status, never thrown.  When a call returns anything but
  *     TRAJ_OK nothing was enqueued (except TRAJ_E_HIP, which reports a failed launch).
  *   - Conditions that only the device can see (a parent array that is not topological)
