@@ -14,7 +14,7 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # GPU tests are skipped (not failed) on hosts without a GPU so that a plain
-    # `pytest` on a CPU machine stays green; `-m gpu` on the GPU machine runs them.
+    # `pytest` on a machine without a GPU stays green; `-m gpu` runs them on an MI355X.
     try:
         import torch
         has_gpu = torch.cuda.is_available()
