@@ -90,6 +90,7 @@ def test_wrong_mask_is_detected(name):
     (33, 2, 0, 2, 2, 128),      # no cache at all
     (64, 3, 65, 6, 2, 128),     # half-draft row blocks, GQA group 3
     (32, 64, 64, 1, 1, 64),     # 64 drafts (deepest chains)
+    (64, 64, 100, 2, 1, 128),   # both maxima: 64 drafts of 64 tokens, a 64-deep chain
     (5, 1, 1, 1, 1, 128),       # single draft, single cache key
 ])
 def test_odd_shapes(L, N, S, Hq, Hkv, D):
