@@ -31,6 +31,7 @@ def _weights(rng, hidden, Hq, Hkv, D, inter):
     (1, 7, 32, 4, 2, 64, 100, 384, [-1, 0, 0, 0, 1, 2, 4]),   # W3D3 hybrid tree, GQA, D 64
     (3, 2, 5, 1, 1, 128, 0, 136, [-1, -1]),                   # no cache, ragged sizes
     (1, 3, 8, 8, 4, 128, 40, 3072, [-1, 0, 1]),               # few rows: split-K projections
+    (1, 64, 64, 2, 1, 128, 50, 256, [-1] + list(range(63))),  # both maxima: a 64-deep chain of 64-token drafts
 ])
 def test_layer_parity(B, N, L, Hq, Hkv, D, S, inter, tree):
     rng = np.random.default_rng(B * 100 + N)
