@@ -112,12 +112,22 @@ static_assert(2 * kR1Loads * (kR1Stages - 2) < 64, "vmcnt has 6 bits");
 // insertion cannot tell which buffer they write and would wait for all of them before every
 // LDS read.  Completion is the caller's explicit s_waitcnt vmcnt; a compiler-tracked load
 // issued earlier only sees stricter waits because of these (loads complete in order).
+// M0 (the LDS destination of the load) is a register the compiler reserves: the statement
+// saves it in a scratch SGPR and restores it after the load, so no code around it sees a
+// changed M0.  On gfx9 an SALU write of M0 needs one wait state before an LDS-DMA load reads
+// it (the compiler's hazard recognizer does not look inside asm), hence the s_nop.
 __device__ __forceinline__ void gemm_dma16(const gemm_i32x4_t& rsrc, unsigned voffset, uint16_t* lds_dst) {
     const unsigned lds = __builtin_amdgcn_readfirstlane((unsigned)(size_t)((gemm_lds_void_t*)lds_dst));
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :
-                 : "s"(lds), "v"(voffset), "s"(rsrc)
-                 : "memory", "m0");
+    unsigned saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(voffset), "s"(rsrc)
+        : "memory");
 }
 
 // Workgroup barrier for a stage ring.  __syncthreads() carries a workgroup release fence,
@@ -176,7 +186,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_ring128_kernel(GemmParam
     auto load_stage = [&](int t, uint16_t* stage) {
         const int k0 = kb + t * kGemmBK;
         const int64_t w_rem = ((int64_t)(ke - k0) * N - n0) * 2;
-        const gemm_i32x4_t wrs = gemm_descriptor(P.W + (int64_t)k0 * N + n0, (unsigned)min(w_rem, kGemmMaxRecords));
+        const gemm_i32x4_t wrs = gemm_descriptor(P.W + (int64_t)k0 * N + n0, (unsigned)(w_rem < kGemmMaxRecords ? w_rem : kGemmMaxRecords));
 #pragma unroll
         for (int j = 0; j < kR1Loads; ++j) {
             const unsigned ao = k0 + a_kc[j] < ke ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
@@ -410,7 +420,7 @@ __global__ __launch_bounds__(kG2Threads, 1) void gemm_tile256_kernel(GemmParams 
         const int64_t w_rem = ((int64_t)(K - k0) * N - n0) * 2;
         const __amdgpu_buffer_rsrc_t wrs =
             __builtin_amdgcn_make_buffer_rsrc((void*)(P.W + (int64_t)k0 * N + n0), (short)0,
-                                              (int)(unsigned)min(w_rem, kGemmMaxRecords), kGemmBufferFlags);
+                                              (int)(unsigned)(w_rem < kGemmMaxRecords ? w_rem : kGemmMaxRecords), kGemmBufferFlags);
 #pragma unroll
         for (int j = 0; j < kG2LoadsPerWave; ++j) {
             const unsigned ao = k0 + a_kc[j] < K ? a_off[j] + 2u * (unsigned)k0 : kGemmOutside;
