@@ -16,9 +16,10 @@ Definitions followed:
   the ones produced by verifying that node.  The children of the committed
   state (parent -1) are checked against the committed state's own conf/idx,
   i.e. the previous step's logits.
-* Verification (Sec. 3.3, "Verification procedure"): a draft block is
-  accepted when its tokens match the model's top predictions; the paper also
-  allows "within top-k / exceed tau" relaxations.  Three readings:
+* Verification (Sec. 3.3, "Verification procedure"): a draft block passes
+  when its tokens agree with the model's best predictions; the section also
+  admits looser checks based on the top-k candidates or on the threshold.
+  Three readings:
     - ``exact`` (default): the child equals step_tau(parent) at every
       position.  A chain of exact acceptances reproduces sequential threshold
       decoding, which is the exactness setting of Theorem 1.

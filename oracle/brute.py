@@ -12,12 +12,14 @@ oracle so that a mistake in one does not repeat in the other:
   paths whose every edge is consistent, and then picks the greedy leaf as the
   lexicographically smallest *maximal* valid path (the walk that always takes
   the lowest-index consistent child ends exactly there) and the longest leaf
-  as the valid endpoint with the largest gain (Sec. 3.3 traversal).
+  as the valid endpoint with the largest gain (Sec. 3.3 traversal).  Edge
+  consistency comes from ``consistent_scalar``, written here from the
+  definitions as set comparisons (it imports nothing from the oracle).
 """
 
 import math
 
-from .accept import MASK, is_consistent
+MASK = -1
 
 
 def _is_on_root_path(j, i, parent_row):
@@ -70,6 +72,35 @@ def attention_scalar(q, k_cache, v_cache, k_draft, v_draft, parent, scale=None, 
     return out
 
 
+def consistent_scalar(child, parent_state, conf, idx, tau, mode="exact"):
+    """Is ``child`` an acceptable next step of ``parent_state`` (Sec. 3.3 verification; Sec. 2.1
+    threshold decoding)?  Written as set comparisons over positions:
+
+    * exact: the positions the child unmasks are exactly the threshold step's set (every masked
+      position whose top-1 confidence is above tau, or, when there is none, the masked position
+      with the largest top-1 confidence, the smaller position on ties), each set to its top-1
+      candidate, and every other position is unchanged;
+    * top1 / topk: no previously unmasked position changes, at least one masked position is
+      unmasked, and each such token is among the first 1 / k candidates of its position.
+    """
+    L = len(parent_state)
+    masked = {p for p in range(L) if parent_state[p] == MASK}
+    unchanged_outside = all(child[p] == parent_state[p] for p in range(L) if p not in masked)
+    newly = {p for p in masked if child[p] != MASK}
+    if not unchanged_outside:
+        return False
+    if mode == "exact":
+        if not masked:
+            return False  # a complete block has no next step
+        chosen = {p for p in masked if conf[p][0] > tau}
+        if not chosen:
+            best = max(float(conf[p][0]) for p in masked)
+            chosen = {min(p for p in masked if float(conf[p][0]) == best)}
+        return newly == chosen and all(child[p] == idx[p][0] for p in chosen)
+    width = {"top1": 1, "topk": len(idx[0])}[mode]
+    return len(newly) >= 1 and all(child[p] in [idx[p][j] for j in range(width)] for p in newly)
+
+
 def _gain(state, committed):
     return sum(1 for p in range(len(committed)) if committed[p] == MASK and state[p] != MASK)
 
@@ -90,7 +121,7 @@ def accept_by_paths(tokens, parent, committed, conf0, idx0, conf, idx, tau, mode
     def edge_ok(c):
         q = int(parent[c])
         C, I = scores(q)
-        return is_consistent(tokens[c], state(q), C, I, tau, mode)
+        return consistent_scalar([int(t) for t in tokens[c]], [int(t) for t in state(q)], C, I, tau, mode)
 
     # all root paths (sequences of drafts starting at a child of -1)
     paths = []

@@ -10,9 +10,10 @@ TEST INFRASTRUCTURE ONLY -- see the package docstring.
   block leaves nothing to speculate on).  The confidences of both blocks come from one
   verification pass whose drafts cover both blocks (2L positions per state).
 * Joint verification (Sec. 3.4 "Joint tree construction", App. D): the trees of B_t (drafts
-  0 .. n_cur-1) and B_{t+1} (drafts n_cur .. n_cur+n_next-1) are verified in one pass; draft
-  tokens of B_{t+1} attend to the root of B_t and vice versa, drafts of one block stay
-  invisible to the other block's non-root drafts.  Returned as per-draft peer bit masks for
+  0 .. n_cur-1) and B_{t+1} (drafts n_cur .. n_cur+n_next-1) are verified in one pass.  Each
+  draft of either tree may additionally look at the root draft of the other tree (the
+  visibility is mutual between the two trees' roots and everything below them); the other
+  tree's non-root drafts stay hidden.  Returned as per-draft peer bit masks for
   the attention oracle's ``peers`` argument.
 """
 

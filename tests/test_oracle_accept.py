@@ -34,12 +34,15 @@ def test_golden_threshold_steps():
 
 
 def test_golden_consistency_modes():
-    g = _load("consistency.json")
-    for case in g["cases"]:
-        for mode in ("exact", "top1", "topk"):
-            got = oracle.is_consistent(np.array(case["child"]), np.array(g["parent_state"]),
-                                       g["conf"], g["idx"], g["tau"], mode)
-            assert got == case[mode], (case["child"], mode)
+    for g in _load("consistency.json")["groups"]:
+        for case in g["cases"]:
+            for mode in ("exact", "top1", "topk"):
+                got = oracle.is_consistent(np.array(case["child"]), np.array(g["parent_state"]),
+                                           g["conf"], g["idx"], g["tau"], mode)
+                assert got == case[mode], (g["note"], case["child"], mode)
+                # the path-enumeration pin carries its own consistency rule: it must agree too
+                alt = brute.consistent_scalar(case["child"], g["parent_state"], g["conf"], g["idx"], g["tau"], mode)
+                assert alt == case[mode], (g["note"], case["child"], mode, "brute")
 
 
 def test_golden_tree_acceptance():
