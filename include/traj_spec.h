@@ -16,9 +16,9 @@
  *   4. traj_build_tree       -- the next step's draft tree from the accepted state
  *                               (Alg. 1: stratification, top-k first level, top-1 deeper,
  *                               pruning by path confidence).
- *   5. traj_interblock_trigger and traj_verify_attn_peers -- inter-block speculation
- *                               (Sec. 3.4): the trigger, and attention for the joint trees of
- *                               two blocks with root-to-root visibility.
+ *   5. traj_interblock_trigger, traj_joint_peers and traj_verify_attn_peers -- inter-block
+ *                               speculation (Sec. 3.4): the trigger, the visibility masks of
+ *                               the joint trees of two blocks, and attention over them.
  *   6. traj_verify_layer     -- a whole decoder layer of the verification forward pass around
  *                               call 1 (norms, projections, RoPE, MLP; synthetic weights),
  *                               traj_refresh_layer, the same layer over whole sequences that
@@ -71,6 +71,7 @@ typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
 #define TRAJ_DEV_BAD_PARENT 0x1 /* some parent[n] was outside [-1, n): treated as -1      */
 #define TRAJ_DEV_BAD_LEAF 0x2   /* traj_build_tree: a leaf outside [-1, n_prev): taken as -1 */
 #define TRAJ_DEV_BAD_BLOCK 0x4  /* some block_start[b] was outside [0, S]: clamped              */
+#define TRAJ_DEV_BAD_ROOT 0x8   /* traj_joint_peers: a root index outside its tree: taken as 0   */
 
 /* ------------------------------------------------------------------------------------
  * 1. Trajectory-masked verification attention  (Sec. 3.3; drafts packed as in Sec. 3.2
@@ -95,9 +96,9 @@ typedef enum { TRAJ_BF16 = 0, TRAJ_F32 = 1 } traj_dtype;
  *         one sequence's cache slice S*Hkv*D*2 bytes below 2 GiB (else TRAJ_E_UNSUPPORTED);
  *         all pointers 16-byte aligned.  RoPE, if any, is already applied by the caller.
  * scale <= 0 selects 1/sqrt(D).
- * workspace: optional device scratch (may be NULL with workspace_bytes 0).  When it is at
- * least traj_verify_attn_workspace_size() bytes the cache keys may be split across more
- * workgroups for small batches; results are identical up to fp32 summation order.
+ * workspace: reserved; the attention kernels use no scratch memory and
+ * traj_verify_attn_workspace_size() returns 0.  The pointer and size are ignored (NULL / 0
+ * are the expected values).
  * out must not alias any input.
  * ------------------------------------------------------------------------------------ */
 typedef struct {
@@ -114,8 +115,8 @@ traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_c
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* traj_verify_attn with per-draft peer visibility  (Sec. 3.4 "Joint tree construction",
- * App. D: when the trees of blocks B_t and B_{t+1} are verified in one pass, draft tokens of
- * B_{t+1} attend to the root of B_t and vice versa).
+ * App. D: the trees of two consecutive blocks verified in one pass, each draft additionally
+ * seeing the root draft of the other block's tree; traj_joint_peers builds those masks).
  * draft_peers [B, N] uint64 (device, may be NULL = traj_verify_attn): bit j of
  * draft_peers[b,n] makes all L tokens of draft j visible to draft n in addition to the cache,
  * itself and its ancestors; one direction per bit (mutual visibility sets both); bits >= N
@@ -125,6 +126,20 @@ traj_status traj_verify_attn_peers(const void* q, const void* k_cache, const voi
                                    const int32_t* draft_parent, const uint64_t* draft_peers,
                                    void* out, const traj_attn_shape* shape,
                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Peer masks of a joint packing for traj_verify_attn_peers  (Sec. 3.4 "Joint tree
+ * construction", App. D).  Per sequence b the drafts [0, n_cur) form the tree of the current
+ * block B_t and the drafts [n_cur, n_cur + n_next) the tree of the next block B_{t+1}; each
+ * draft of B_t's tree sees the root draft of B_{t+1}'s tree and each draft of B_{t+1}'s tree
+ * sees the root draft of B_t's tree:
+ *     peers[b, n] = 1 << (n_cur + root_next[b])   for n <  n_cur,
+ *     peers[b, n] = 1 << root_cur[b]              for n >= n_cur.
+ * root_cur [B] (in [0, n_cur)) and root_next [B] (in [0, n_next)) are int32 device arrays or
+ * NULL (root 0); a root outside its tree is taken as 0 and sets TRAJ_DEV_BAD_ROOT.
+ * peers: [B, n_cur + n_next] uint64 device output.
+ * Limits: B >= 1; n_cur >= 1; n_next >= 1; n_cur + n_next <= 64. */
+traj_status traj_joint_peers(int32_t B, int32_t n_cur, int32_t n_next, const int32_t* root_cur,
+                             const int32_t* root_next, uint64_t* peers, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * 2. Confidence and top-k candidates  (Sec. 3.2, Eq. 2; "Candidate collection")
@@ -382,7 +397,9 @@ traj_status traj_linear(const void* x, const void* w, void* y, int64_t M, int64_
  * ------------------------------------------------------------------------------------ */
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* traj_status_string(int32_t status);
-/* Static version string of the library. */
+/* Static version string of the library: "libtrajspec <version> gfx950 sources <sha256>", the
+ * digest of the sources and compiler flags it was built from ("unstamped" when built without
+ * the package's build script). */
 const char* traj_version(void);
 /* Synchronises `stream`, copies the current device's status word (TRAJ_DEV_* bits) to
  * *host_flags and, if reset != 0, clears it.  Returns TRAJ_E_HIP on a runtime error. */

@@ -18,8 +18,9 @@ and the next step's drafts:
 and inter-block speculation (Sec. 3.4):
 
 * :func:`interblock_trigger` -- whether the next block is confident enough to
-  speculate on both blocks; :func:`verify_attn` with ``peers`` (see
-  :func:`joint_peers`) verifies the joint trees with root-to-root visibility.
+  speculate on both blocks; :func:`joint_peers` builds the visibility masks of the
+  two blocks' joint trees on the device and :func:`verify_attn` with ``peers``
+  verifies them in one pass.
 
 and :func:`verify_layer`, a whole decoder layer of the verification forward pass around the
 attention (norms, projections on the library's MFMA GEMM, RoPE, SwiGLU MLP), and
@@ -29,12 +30,15 @@ sequences at a block boundary and refreshes the dual cache (App. A).
 
 from ._lib import (  # noqa: F401
     DEV_BAD_BLOCK,
+    DEV_BAD_ROOT,
     DEV_BAD_LEAF,
     DEV_BAD_PARENT,
     LIB_PATH,
     TrajSpecError,
     accept,
     build_tree,
+    built_digest,
+    check_build,
     confidence_topk,
     confidence_topk_workspace_size,
     device_status,

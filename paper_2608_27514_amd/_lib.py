@@ -8,8 +8,6 @@ If the library is not built the calls raise -- there is no fallback.
 import ctypes
 import os
 
-import numpy as np
-
 import torch
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -24,6 +22,7 @@ TRAVERSALS = {"greedy": 0, "longest": 1}
 DEV_BAD_PARENT = 0x1
 DEV_BAD_LEAF = 0x2
 DEV_BAD_BLOCK = 0x4
+DEV_BAD_ROOT = 0x8
 
 
 class TrajSpecError(RuntimeError):
@@ -89,6 +88,7 @@ EXPORTS = {
                                      ctypes.POINTER(Accepted), ctypes.c_void_p]),
     "traj_verify_attn_peers": (ctypes.c_int32, [ctypes.c_void_p] * 8 + [ctypes.POINTER(AttnShape), ctypes.c_void_p,
                                                                          ctypes.c_size_t, ctypes.c_void_p]),
+    "traj_joint_peers": (ctypes.c_int32, [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 4),
     "traj_interblock_trigger": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                  ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_void_p, ctypes.c_void_p]),
@@ -135,6 +135,22 @@ def load():
 
 def version():
     return _lib().traj_version().decode()
+
+
+def built_digest():
+    """Source digest the loaded library was built from (stamped into traj_version())."""
+    return version().rsplit(" ", 1)[-1]
+
+
+def check_build():
+    """Raise unless the loaded library was built from the sources checked out next to it."""
+    from .build import source_digest
+    want = source_digest()
+    got = built_digest()
+    if got != want:
+        raise RuntimeError(f"{LIB_PATH} was built from other sources (digest {got[:16]}, sources {want[:16]}); "
+                           "rebuild with `python -m paper_2608_27514_amd.build`")
+    return got
 
 
 def _check(status, where):
@@ -204,18 +220,24 @@ def verify_attn(q, k_cache, v_cache, k_draft, v_draft, draft_parent, out=None, s
     return out
 
 
-def joint_peers(n_cur, n_next, root_cur=0, root_next=0):
-    """Host-side peer masks for the joint trees of two blocks packed as drafts
-    [0, n_cur) (block t) and [n_cur, n_cur + n_next) (block t+1): every draft of block t+1
-    sees block t's root draft and every draft of block t sees block t+1's root draft.
-    Returns a [n_cur + n_next] int64 CPU tensor holding the uint64 bit masks."""
-    n = n_cur + n_next
-    if not (0 <= root_cur < n_cur and 0 <= root_next < n_next and n <= 64):
-        raise ValueError("roots must index their trees and n_cur + n_next <= 64")
-    bits = np.zeros(n, dtype=np.uint64)
-    bits[:n_cur] |= np.uint64(1) << np.uint64(n_cur + root_next)
-    bits[n_cur:] |= np.uint64(1) << np.uint64(root_cur)
-    return torch.from_numpy(bits.view(np.int64).copy())
+def joint_peers(B, n_cur, n_next, root_cur=None, root_next=None, out=None, device=None, stream=None):
+    """Peer masks of a joint packing (traj_joint_peers): drafts [0, n_cur) hold block t's
+    tree, [n_cur, n_cur + n_next) block t+1's; root_cur / root_next are [B] int32 device
+    tensors (None = root 0).  Returns a [B, n_cur + n_next] int64 device tensor holding the
+    uint64 bit masks traj_verify_attn_peers takes."""
+    for name, t in (("root_cur", root_cur), ("root_next", root_next)):
+        if t is not None:
+            _dev(t, name, torch.int32)
+            if t.numel() != B:
+                raise ValueError(f"{name} must hold B entries")
+    if out is None:
+        dev = device or (root_cur.device if root_cur is not None else
+                         root_next.device if root_next is not None else torch.device("cuda"))
+        out = torch.empty((B, n_cur + n_next), dtype=torch.int64, device=dev)
+    _dev(out, "out", torch.int64)
+    _check(_lib().traj_joint_peers(B, n_cur, n_next, _ptr(root_cur), _ptr(root_next), _ptr(out), _stream(stream)),
+           "traj_joint_peers")
+    return out
 
 
 def interblock_trigger(state, conf, threshold, out=None, stream=None):

