@@ -159,31 +159,55 @@ def run_step(x, buf, tau, stream, ev=None):
         ev[3].record(stream)
 
 
+def cpu_workers():
+    """Host threads for the oracle: the process's CPU affinity set, capped at the 16-core
+    share of one GPU on the shared hosts this runs on."""
+    return max(1, min(len(os.sched_getaffinity(0)), 16))
+
+
 def cpu_baseline(x, buf, wl, tau, n_seq):
-    """The oracle, as it stands, on the first n_seq sequences of the same inputs; also
-    checks the GPU outputs of those sequences against it."""
+    """The oracle, as it stands, on the first n_seq sequences of the same inputs, run on a pool
+    of host threads (one BLAS thread each; numpy releases the interpreter lock in its array
+    kernels): attention one query head per task, the logit pass in equal contiguous row ranges,
+    acceptance as one call.  Also checks the GPU outputs of those sequences against it."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        blas_threads = 1
+    from threadpoolctl import threadpool_limits
+    workers = cpu_workers()
     sl = slice(0, n_seq)
     f64 = lambda t: t[sl].float().cpu().numpy().astype(np.float64)  # noqa: E731
     q, kc, vc, kd, vd = (f64(t) for t in (x.q, x.kc, x.vc, x.kd, x.vd))
     rows = n_seq * wl.N * wl.L
     lg = x.logits[:rows].float().cpu().numpy()
     parent = x.d["parent"][sl]
-    t0 = time.perf_counter()
-    ref_out = oracle.verify_attention(q, kc, vc, kd, vd, parent)
-    t1 = time.perf_counter()
-    rc, ri = oracle.confidence_topk(lg, wl.k)
-    t2 = time.perf_counter()
-    shp = (n_seq, wl.N, wl.L, wl.k)
-    ref_acc = oracle.accept_batch(x.d["tokens"][sl], parent, x.d["committed"][sl],
-                                  x.d["conf0"][sl].astype(np.float64), x.d["idx0"][sl], rc.reshape(shp),
-                                  ri.reshape(shp), tau)
-    t3 = time.perf_counter()
+    G = wl.Hq // wl.Hkv
+    ref_out = np.empty(q.shape, dtype=np.float64)
+
+    def attn_head(h):
+        g = h // G
+        ref_out[:, :, :, h:h + 1] = oracle.verify_attention(q[:, :, :, h:h + 1], kc[:, :, g:g + 1], vc[:, :, g:g + 1],
+                                                            kd[:, :, :, g:g + 1], vd[:, :, :, g:g + 1], parent)
+
+    bounds = np.linspace(0, rows, workers + 1).astype(int)
+    parts = [None] * workers
+
+    def conf_part(i):
+        parts[i] = oracle.confidence_topk(lg[bounds[i]:bounds[i + 1]], wl.k)
+
+    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+        t0 = time.perf_counter()
+        list(ex.map(attn_head, range(wl.Hq)))
+        t1 = time.perf_counter()
+        list(ex.map(conf_part, range(workers)))
+        rc = np.concatenate([p_[0] for p_ in parts])
+        ri = np.concatenate([p_[1] for p_ in parts])
+        t2 = time.perf_counter()
+        shp = (n_seq, wl.N, wl.L, wl.k)
+        ref_acc = oracle.accept_batch(x.d["tokens"][sl], parent, x.d["committed"][sl],
+                                      x.d["conf0"][sl].astype(np.float64), x.d["idx0"][sl], rc.reshape(shp),
+                                      ri.reshape(shp), tau)
+        t3 = time.perf_counter()
     # sample parity of the timed GPU outputs
     g_out = buf.out[sl].float().cpu().numpy()
     attn_ok = bool((np.abs(g_out - ref_out) <= 2e-3 + 2e-2 * np.abs(ref_out)).all())
@@ -196,16 +220,58 @@ def cpu_baseline(x, buf, wl, tau, n_seq):
     return {
         "value": rows / total,
         "unit": "tokens/s",
-        "cores": int(blas_threads),
+        "cores": workers,
         "kind": "oracle",
         "sample": (f"first {n_seq} of {wl.B} sequences ({rows} draft tokens: all {wl.Hq} heads of "
-                   f"attention, {rows} logit rows, acceptance); fp64 numpy, BLAS threads={blas_threads}, "
-                   f"other parts single-threaded"),
+                   f"attention, {rows} logit rows, acceptance); fp64 numpy on a pool of {workers} host threads "
+                   f"(affinity set {len(os.sched_getaffinity(0))} CPUs), one BLAS thread each"),
+        "pool": {"threads": workers, "attention_tasks": wl.Hq, "logit_tasks": workers, "accept_tasks": 1},
         "seconds": {"attention": t1 - t0, "confidence_topk": t2 - t1, "accept": t3 - t2, "total": total},
         "sample_parity": {"attention_within_tol": attn_ok, "topk_idx_exact": idx_ok,
                           "conf_max_abs_err": conf_err, "leaf_exact": leaf_ok,
                           "fragile_sequences_excluded": fragile},
     }
+
+
+def sharp_sample_parity(wl, parent, stream, b=None, h=None):
+    """The timed attention launch (full batch and heads, the workload's parent array) on sharp
+    inputs (q ~ 3 N(0,1), k, v ~ N(0,1)), where a wrong mask moves outputs far outside the
+    tolerance: one sampled (sequence, head) slice is checked against the oracle, and the same slice
+    must fail against oracles with a wrong mask (ancestors dropped; siblings chained)."""
+    import oracle
+    from synthetic import attention_inputs as ai
+    seed = seed_for(wl.cid, salt=3)
+    q, kc, vc, kd, vd = ai(wl, seed, "sharp", device="cuda")
+    out = tsp.verify_attn(q, kc, vc, kd, vd, torch.as_tensor(parent, dtype=torch.int32, device="cuda"),
+                          stream=stream)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(seed)
+    b = int(rng.integers(wl.B)) if b is None else b
+    h = int(rng.integers(wl.Hq)) if h is None else h
+    g = h // (wl.Hq // wl.Hkv)
+    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    sub = [f64(q[b:b + 1, :, :, h:h + 1]), f64(kc[b:b + 1, :, g:g + 1]), f64(vc[b:b + 1, :, g:g + 1]),
+           f64(kd[b:b + 1, :, :, g:g + 1]), f64(vd[b:b + 1, :, :, g:g + 1])]
+    got = f64(out[b:b + 1, :, :, h:h + 1])
+    del q, kc, vc, kd, vd, out
+
+    def within(par):
+        ref = oracle.verify_attention(*sub, par)
+        aw = oracle.verify_attention(sub[0], sub[1], np.abs(sub[2]), sub[3], np.abs(sub[4]), par)
+        lim = 2e-3 + 2e-2 * np.abs(ref) + 2 * 2.0 ** -9 * aw
+        bad = np.abs(got - ref) > lim
+        return (not bad.any()), float(bad.mean())
+
+    pr = np.asarray(parent)[b:b + 1]
+    ok, _ = within(pr)
+    wrong = {"siblings_chained": np.arange(-1, wl.N - 1, dtype=np.int32)[None]}
+    if (pr >= 0).any():
+        wrong["ancestors_dropped"] = np.full_like(pr, -1)
+    rejected = {}
+    for name, wp in wrong.items():
+        ok_w, frac_w = within(wp)
+        rejected[name] = {"rejected": not ok_w, "fraction_outside": frac_w}
+    return {"sequence": b, "head": h, "within_sharp_bound": ok, "wrong_masks": rejected}
 
 
 def time_warm(x, buf, tau, stream, steps):
@@ -226,6 +292,87 @@ def time_warm(x, buf, tau, stream, steps):
          for a, name in enumerate(("verify_attn", "confidence_topk", "accept"))}
     wl = x.wl
     return {"ms_per_step": ms, "tokens_per_s": wl.B * wl.N * wl.L / (ms * 1e-3), "kernels_ms": k}
+
+
+def time_steps(copies, buf, tau, stream, steps, warmup):
+    """W warm-up steps, then K steps over the rotated input copies between two synchronisations,
+    HIP events recorded on the launch stream around every call.  Returns (ms per step, per-kernel
+    ms averages)."""
+    n = len(copies)
+    for i in range(warmup):
+        run_step(copies[i % n], buf, tau, stream)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(steps):
+        run_step(copies[i % n], buf, tau, stream, evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    kernels = {name: sum(e[a].elapsed_time(e[a + 1]) for e in evs) / steps
+               for a, name in enumerate(("verify_attn", "confidence_topk", "accept"))}
+    return start.elapsed_time(stop) / steps, kernels
+
+
+def make_copies(wl, tau, dev):
+    """Input copies rotated through the timed steps so that together they exceed twice the
+    256 MB Infinity Cache and every step reads its inputs from HBM."""
+    seed = seed_for(wl.cid)
+    x = StepInputs(wl, seed, tau, dev)
+    copies = [x]
+    n_copies = max(1, min(8, math.ceil(2 * MALL_BYTES / x.nbytes())))
+    for c in range(1, n_copies):
+        copies.append(StepInputs(wl, seed + 101 * c, tau, dev))
+    return copies
+
+
+def describe(wl, tau):
+    return (f"{wl.name}: B{wl.B} N{wl.N} L{wl.L} Hq{wl.Hq} Hkv{wl.Hkv} D{wl.D} S{wl.S}({wl.S_prefix}+{wl.S_suffix}) "
+            f"V{wl.V} {wl.logits_dtype} logits, k{wl.k}, tau {tau}")
+
+
+def step_record(wl, x, ms_step, kernels, n_copies, steps):
+    """Throughput and roofline fractions of one workload's timed steps."""
+    flops = attn_flops(wl, x.d["parent"])
+    t_attn, t_conf = kernels["verify_attn"], kernels["confidence_topk"]
+    a_tflops = flops / (t_attn * 1e-3) / 1e12
+    a_gbs = attn_bytes(wl) / (t_attn * 1e-3) / 1e9
+    l_gbs = logit_bytes(wl) / (t_conf * 1e-3) / 1e9
+    return {
+        "workload": describe(wl, wl.tau),
+        "draft_tokens_per_step": wl.B * wl.N * wl.L,
+        "input_copies_rotated": n_copies,
+        "steps": steps,
+        "step_us": ms_step * 1e3,
+        "tokens_per_s": wl.B * wl.N * wl.L / (ms_step * 1e-3),
+        "kernel_us": {k: v * 1e3 for k, v in kernels.items()},
+        "verify_attn": {"algorithmic_flop_per_launch": flops, "tflops": a_tflops,
+                        "frac_of_bf16_peak": a_tflops / PEAK_BF16_TFLOPS,
+                        "algorithmic_bytes_per_launch": attn_bytes(wl), "gbs": a_gbs,
+                        "frac_of_hbm": a_gbs / PEAK_HBM_GBS,
+                        "bound": "hbm" if flops / attn_bytes(wl) < PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "mfma"},
+        "logit_pass": {"algorithmic_bytes_per_launch": logit_bytes(wl), "gbs": l_gbs,
+                       "frac_of_hbm": l_gbs / PEAK_HBM_GBS},
+    }
+
+
+def time_config(cid, stream, steps, warmup):
+    """A workload other than the headline one, timed in the same run exactly as the headline step
+    (rotated copies, per-kernel HIP events on the launch stream)."""
+    wl = WORKLOADS[cid]
+    dev = torch.device("cuda:0")
+    copies = make_copies(wl, wl.tau, dev)
+    buf = Buffers(wl, dev, copies[0].logits)
+    torch.cuda.synchronize()
+    ms_step, kernels = time_steps(copies, buf, wl.tau, stream, steps, warmup)
+    rec = step_record(wl, copies[0], ms_step, kernels, len(copies), steps)
+    run_step(copies[0], buf, wl.tau, stream)
+    torch.cuda.synchronize()
+    rec["accepted_tokens_per_step"] = float(buf.acc["n_accepted"].sum().item())
+    del copies, buf
+    torch.cuda.empty_cache()
+    return rec
 
 
 TREE_WIDTH, TREE_DEPTH = 3, 3  # the paper's adopted W3D3 hybrid tree
@@ -261,7 +408,7 @@ def time_interblock(x, buf, tau, stream, reps=5, trig_reps=50):
     n_next = min(4, wl.N - 1)
     if n_next < 1:
         return None
-    peers = tsp.joint_peers(wl.N - n_next, n_next).to(x.q.device).repeat(wl.B, 1).contiguous()
+    peers = tsp.joint_peers(wl.B, wl.N - n_next, n_next, device=x.q.device, stream=stream)
     scratch = torch.empty_like(buf.out)  # buf.out stays the step's output
     times = {"plain": 0.0, "peers": 0.0}
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2 * reps)]
@@ -534,6 +681,11 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the measurements beside the step (warm cache, tree build, inter-block), e.g. "
                          "for a kernel trace of the step alone")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip timing the other workloads (the 'configs' record)")
+    ap.add_argument("--config-steps", type=int, default=50, help="timed steps of each other workload")
+    ap.add_argument("--no-sharp-parity", action="store_true",
+                    help="skip the sharp-input attention check at the timed launch")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run three 1 GiB device-to-device copies (for scaling rocprofv3 FETCH_SIZE / "
                          "WRITE_SIZE readings) and exit")
@@ -561,34 +713,14 @@ def main():
     tau = wl.tau if args.tau is None else args.tau
     dev = torch.device("cuda:0")
     seed = seed_for(wl.cid)
-    x = StepInputs(wl, seed, tau, dev)
-    copies = [x]
-    per_copy = x.nbytes()
-    n_copies = max(1, min(8, math.ceil(2 * MALL_BYTES / per_copy)))
-    for c in range(1, n_copies):
-        copies.append(StepInputs(wl, seed + 101 * c, tau, dev))
+    copies = make_copies(wl, tau, dev)
+    x = copies[0]
+    n_copies = len(copies)
     buf = Buffers(wl, dev, x.logits)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
-
-    for i in range(args.warmup):
-        run_step(copies[i % n_copies], buf, tau, stream)
-    torch.cuda.synchronize()
-
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        run_step(copies[i % n_copies], buf, tau, stream, evs[i])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_step = ms_total / args.steps
-    t_attn = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-    t_conf = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-    t_acc = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    ms_step, kern = time_steps(copies, buf, tau, stream, args.steps, args.warmup)
+    t_attn, t_conf, t_acc = kern["verify_attn"], kern["confidence_topk"], kern["accept"]
 
     tokens = wl.B * wl.N * wl.L
     flops = attn_flops(wl, x.d["parent"])
@@ -605,6 +737,13 @@ def main():
     refresh = None if args.no_extras else time_refresh(wl, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     forward = None if args.no_extras else time_forward_one_sequence(wl, stream)
+    sharp = None if args.no_sharp_parity else sharp_sample_parity(wl, x.d["parent"], stream)
+    configs = None
+    if not args.no_configs:
+        configs = {}
+        for cid in sorted(WORKLOADS):
+            if cid != wl.cid:
+                configs[WORKLOADS[cid].name] = time_config(cid, stream, args.config_steps, args.warmup)
     status = tsp.device_status(reset=True)
 
     result = {
@@ -621,9 +760,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded; stands in for the paper's benchmarks and LLaDA/Dream activations)",
         "config": {
-            "workload": f"{wl.name}: B{wl.B} N{wl.N} L{wl.L} Hq{wl.Hq} Hkv{wl.Hkv} D{wl.D} "
-                        f"S{wl.S}({wl.S_prefix}+{wl.S_suffix}) V{wl.V} {wl.logits_dtype} logits, k{wl.k}, "
-                        f"tau {tau}",
+            "workload": describe(wl, tau),
             "draft_tokens_per_step": tokens,
             "tree": "levels " + "+".join(map(str, wl.level_sizes)) if wl.level_sizes else "explicit parents",
             "input_copies_rotated": n_copies,
@@ -655,6 +792,10 @@ def main():
         "forward_one_sequence": forward,
         "device_status": status,
     }
+    if configs is not None:
+        result["configs"] = configs
+    if sharp is not None:
+        result["attention_sharp_parity"] = sharp
     if wl.cid == 5 and not args.no_sweep:
         for t2 in (0.7, 0.8):
             x.replant(seed, t2)

@@ -4,6 +4,10 @@ Tolerance: |gpu - oracle| <= 2e-3 + 2e-2 |oracle| elementwise (bf16 inputs,
 fp32 accumulation, bf16 output).  Besides the spec-distributed inputs
 (N(0,1)/sqrt(D), nearly uniform attention) every shape is also run "sharp"
 (q ~ 3 N(0,1), k, v ~ N(0,1)), where a wrong mask is far outside tolerance.
+With spec inputs at the full cache lengths the weights are nearly uniform over
+thousands of keys and a dropped ancestor block stays inside the tolerance, so
+the full-size launches are checked on sharp inputs together with wrong-mask
+negative controls (test_full_size_sharp_sampled_heads_and_wrong_masks).
 """
 
 import numpy as np
@@ -161,6 +165,43 @@ def test_full_size_sampled_heads(cid):
         ref = _oracle(sub, parent[b:b + 1])
         ok, worst, frac = attn_close(out[b:b + 1, :, :, h:h + 1], ref)
         assert ok, f"{wl.name} b={b} h={h}: worst {worst:.3g} frac {frac:.3%}"
+
+
+def _wrong_parents(parent, N):
+    """Negative controls: every ancestor dropped (when the tree has any), and siblings made
+    visible by chaining every draft to its predecessor."""
+    out = {"siblings_chained": np.tile(np.arange(-1, N - 1, dtype=np.int32), (parent.shape[0], 1))}
+    if (parent >= 0).any():
+        out["ancestors_dropped"] = np.full_like(parent, -1)
+    return out
+
+
+@pytest.mark.parametrize("cid", [2, 3, 4, 5])
+def test_full_size_sharp_sampled_heads_and_wrong_masks(cid):
+    """The timed launch (full batch, all heads, the workload's parent array) on sharp inputs
+    (q ~ 3 N(0,1), k, v ~ N(0,1)): sampled (sequence, query head) slices must match the oracle
+    within the sharp-input bound, and the same GPU slices must FAIL that bound against an oracle
+    with a wrong mask (ancestors dropped; siblings chained), so a mask error cannot pass here."""
+    wl = WORKLOADS[cid]
+    q, kc, vc, kd, vd = attention_inputs(wl, seed_for(cid, 3), "sharp", device="cuda")
+    parent = _parents(wl, seed_for(cid))
+    out = tsp.verify_attn(q, kc, vc, kd, vd, cuda(parent, torch.int32))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(100 + cid)
+    G = wl.Hq // wl.Hkv
+    picks = [(0, 0), (wl.B - 1, wl.Hq - 1)] + [(int(rng.integers(wl.B)), int(rng.integers(wl.Hq))) for _ in range(3)]
+    wrong = _wrong_parents(parent, wl.N)
+    for b, h in picks:
+        g = h // G
+        sub = [q[b:b + 1, :, :, h:h + 1], kc[b:b + 1, :, g:g + 1], vc[b:b + 1, :, g:g + 1],
+               kd[b:b + 1, :, :, g:g + 1], vd[b:b + 1, :, :, g:g + 1]]
+        got = out[b:b + 1, :, :, h:h + 1]
+        ok, worst, frac = _check(got, sub, parent[b:b + 1], "sharp")
+        assert ok, f"{wl.name} b={b} h={h}: worst excess {worst:.3g}, {frac:.3%} outside"
+        for name, wp in wrong.items():
+            ok_w, _, frac_w = _check(got, sub, wp[b:b + 1], "sharp")
+            assert not ok_w, f"{wl.name} b={b} h={h}: the GPU output also matches a mask with {name}"
+            assert frac_w > 0.01, f"{wl.name} b={b} h={h} {name}: only {frac_w:.3%} outside"
 
 
 def test_invalid_parent_is_flagged_and_bounded():

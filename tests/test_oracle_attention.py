@@ -16,6 +16,7 @@ import torch
 
 import oracle
 from oracle import brute
+from synthetic import WORKLOADS, attention_inputs, decode_inputs, seed_for
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -173,3 +174,26 @@ def test_bad_parent_arrays_are_rejected():
         oracle.ancestor_sets([-1, 2, 0])
     with pytest.raises(ValueError):
         oracle.ancestor_sets([-2])
+
+
+@pytest.mark.parametrize("cid", [3, 4, 5])
+def test_full_shape_sharp_inputs_tell_masks_apart(cid):
+    """Discriminating power of the full-size GPU check: on one (sequence, head) slice of the
+    workload's real shape (cache length, drafts, tree) with sharp inputs, an oracle with a wrong
+    mask (ancestors dropped; siblings chained) differs from the right one by more than the
+    sharp-input bound on a sizeable share of the elements."""
+    from helpers import attn_close
+    wl = WORKLOADS[cid]
+    parent = decode_inputs(wl.with_(V=64), seed_for(cid))["parent"][:1]
+    one = wl.with_(B=1, Hq=wl.Hq // wl.Hkv, Hkv=1)
+    q, kc, vc, kd, vd = [t.float().numpy().astype(np.float64) for t in attention_inputs(one, 500 + cid, "sharp")]
+    q = q[:, :, :, :1]
+    ref = oracle.verify_attention(q, kc, vc, kd, vd, parent)
+    wrong = {"siblings_chained": np.arange(-1, wl.N - 1, dtype=np.int32)[None]}
+    if (parent >= 0).any():
+        wrong["ancestors_dropped"] = np.full_like(parent, -1)
+    for name, wp in wrong.items():
+        bad = oracle.verify_attention(q, kc, vc, kd, vd, wp)
+        aw = oracle.verify_attention(q, kc, np.abs(vc), kd, np.abs(vd), wp)
+        ok, _, frac = attn_close(ref, bad, aw)
+        assert not ok and frac > 0.05, (name, frac)
