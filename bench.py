@@ -67,6 +67,11 @@ def measured_traffic(kernel, workload):
     return rec["bytes_per_launch"]
 
 
+def log(msg):
+    """Progress on stderr (the result line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def depths(parent_row):
     out = []
     for n in range(len(parent_row)):
@@ -713,13 +718,16 @@ def main():
     tau = wl.tau if args.tau is None else args.tau
     dev = torch.device("cuda:0")
     seed = seed_for(wl.cid)
+    log(f"inputs: {wl.name}")
     copies = make_copies(wl, tau, dev)
     x = copies[0]
     n_copies = len(copies)
     buf = Buffers(wl, dev, x.logits)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
     ms_step, kern = time_steps(copies, buf, tau, stream, args.steps, args.warmup)
+    log(f"step {ms_step:.4f} ms")
     t_attn, t_conf, t_acc = kern["verify_attn"], kern["confidence_topk"], kern["accept"]
 
     tokens = wl.B * wl.N * wl.L
@@ -731,18 +739,23 @@ def main():
     run_step(x, buf, tau, stream)
     torch.cuda.synchronize()
     acc_main = buf.acc["n_accepted"].cpu().numpy()
+    if not args.no_extras:
+        log("extras: tree build, layer, refresh, inter-block, one-sequence forward")
     tree = None if args.no_extras else time_tree_build(x, buf, tau, stream)
     layer = None if args.no_extras else time_layer(x, stream)
     layer_one = None if args.no_extras else time_layer_one_sequence(wl, stream)
     refresh = None if args.no_extras else time_refresh(wl, stream)
     inter = None if args.no_extras else time_interblock(x, buf, tau, stream)
     forward = None if args.no_extras else time_forward_one_sequence(wl, stream)
+    if not args.no_sharp_parity:
+        log("sharp-input attention check at the timed launch")
     sharp = None if args.no_sharp_parity else sharp_sample_parity(wl, x.d["parent"], stream)
     configs = None
     if not args.no_configs:
         configs = {}
         for cid in sorted(WORKLOADS):
             if cid != wl.cid:
+                log(f"config {WORKLOADS[cid].name}")
                 configs[WORKLOADS[cid].name] = time_config(cid, stream, args.config_steps, args.warmup)
     status = tsp.device_status(reset=True)
 
@@ -808,6 +821,7 @@ def main():
         run_step(x, buf, tau, stream)
         torch.cuda.synchronize()
     if not args.no_cpu_baseline:
+        log("oracle baseline on the host")
         result["cpu_baseline"] = cpu_baseline(x, buf, wl, tau, min(args.cpu_sample_seqs, wl.B))
     print(json.dumps(result), flush=True)
 
