@@ -681,7 +681,7 @@ def main():
     ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-seqs", type=int, default=1)
+    ap.add_argument("--cpu-sample-seqs", type=int, default=8)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the measurements beside the step (warm cache, tree build, inter-block), e.g. "

@@ -3,26 +3,36 @@
 // first on equal values) and conf_j = exp(l_j - m) / s.
 //
 // HBM-bound streaming design for gfx950:
-//   * one 256-thread workgroup streams one row (or one slice of a row when there are too
-//     few rows to fill 256 CUs) with 16-byte non-temporal loads: full sweeps of the
-//     workgroup load unconditionally, two vectors per lane per sweep, and the next sweep's
-//     loads are issued before the current sweep is absorbed (a guard per load would put each
-//     load in its own branch and serialise them); only the last, partial sweep checks bounds;
-//   * each lane keeps a running (max, rescaled sum) and a sorted top-K list; a vector of 8
-//     bf16 costs one max-tree, one rescale test, 8 fma+exp2+add and one compare against
-//     the lane's current K-th value (insertions are rare after the first few vectors);
-//   * lanes merge through cross-lane shuffles, waves through LDS; row slices write
-//     (max, sum, top-K) partials that a second one-wave-per-row kernel merges with the
-//     same associative rule.
+//   * one workgroup streams one row (or one slice of a row when there are very few rows) with
+//     16-byte non-temporal loads held in a register ring: DEPTH sweeps of U vectors per lane,
+//     DEPTH - 1 of them in flight while one is absorbed.  The main loop runs whole groups of
+//     DEPTH sweeps with unconditional loads (past the end a lane reloads the last sweep and
+//     discards it), so the compiler's load waits count exactly the older loads;
+//   * the workgroup size follows the row count: one wave per row for large batches (many
+//     resident workgroups per CU), 2 or 8 waves per row for short batches so that the launch
+//     still holds about two waves per SIMD;
+//   * per lane a lazily moved reference value r (an element of the lane, raised only when a
+//     vector maximum exceeds it by 2^8 in the exp2 domain: a wave-uniform branch that is rare
+//     after the first vectors) with the running sum of exp2((x - r) log2e); a vector costs its
+//     unpack, a 3-input maximum tree, one FMA + one exp2 + one add per value and two compares;
+//   * the top-k candidates live in a per-lane sorted list of 64-bit keys (order-preserving value
+//     bits, ~index) whose merges are unsigned max/min; a vector takes the insertion path only
+//     when its maximum reaches max(wave floor, the lane's k-th key), kept as one float.  The wave
+//     floor is a lower bound on the row's k-th largest value (the k-th largest lane maximum),
+//     first taken from sweep 0 before anything is absorbed, then after sweeps 1, 3, 7, ...;
+//   * lanes merge (reference, sum) by shuffles and their keys by k rounds of a wave-wide
+//     maximum, waves through LDS; row slices write (reference, sum, top-K) partial records that
+//     a second one-wave-per-row kernel merges with the same associative rule.
 #pragma once
 
 #include "common.hpp"
 
 namespace trajspec {
 
-constexpr int kTopkThreads = 256;
-constexpr int kTopkUnroll = 2;
-constexpr int kTopkRecord = 2 + 2 * 8;  // floats per partial record: m, s, 8 64-bit keys
+constexpr int kTopkRecord = 2 + 2 * 8;  // floats per partial record: reference, sum, 8 64-bit keys
+// The lazy reference moves when a value exceeds it by this much in the exp2 domain, so every
+// term of a lane's sum stays below 2^kTopkLazyLog2 relative to its reference.
+constexpr float kTopkLazyLog2 = 8.0f;
 
 // A candidate is packed into one 64-bit key whose unsigned order is the selection order:
 // high word = order-preserving image of the fp32 value (-0 folded onto +0), low word =
@@ -42,6 +52,12 @@ __device__ __forceinline__ float key_value(uint64_t k) { return value_of_bits((u
 __device__ __forceinline__ int key_index(uint64_t k) { return (int)(~(uint32_t)k); }
 __device__ __forceinline__ uint64_t kmax(uint64_t a, uint64_t b) { return a > b ? a : b; }
 __device__ __forceinline__ uint64_t kmin(uint64_t a, uint64_t b) { return a > b ? b : a; }
+
+// Float threshold equivalent to "order_bits(x) >= b" for non-NaN x: every image at or below
+// that of -inf (0x007fffff; in practice the empty key 0) accepts all values.
+__device__ __forceinline__ float threshold_of_bits(uint32_t b) {
+    return b <= 0x007fffffu ? kNegInf : value_of_bits(b);
+}
 
 template <int K>
 struct TopList {
@@ -87,8 +103,8 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int off) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Merge two (max, sum) pairs expressed in log2-domain-free form: sums are relative to
-// their own max; the result is relative to the larger max.
+// Merge two (reference, sum) pairs, each sum relative to its own reference; the result is
+// relative to the larger reference.
 __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
     const float M = fmaxf(m, m2);
     const float Ms = fmaxf(M, -1e30f);
@@ -96,55 +112,11 @@ __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2)
     m = M;
 }
 
-template <int K>
-__device__ __forceinline__ void wave_merge(float& m, float& s, TopList<K>& tl) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const float m2 = __shfl_xor(m, off);
-        const float s2 = __shfl_xor(s, off);
-        merge_ms(m, s, m2, s2);
-        uint64_t o[K];
-#pragma unroll
-        for (int j = 0; j < K; ++j) o[j] = shfl_xor64(tl.key[j], off);
-        tl.merge(o);
-    }
-}
-
-// Running update with one vector of NV values starting at vocabulary index id0.
-// `floor_bits` is a lower bound (order_bits form) on the row's k-th largest value shared by
-// the wave: values below it can never reach the row's top-k, so only vectors holding a
-// value >= max(floor, this lane's K-th) take the insertion path.
-template <int K, int NV>
-__device__ __forceinline__ void absorb(const float (&x)[NV], int id0, float& m, float& s, TopList<K>& tl,
-                                       uint32_t floor_bits) {
-    float vmax = x[0];
-#pragma unroll
-    for (int j = 1; j < NV; ++j) vmax = fmaxf(vmax, x[j]);
-    if (vmax > m) {
-        s *= fast_exp2((m - vmax) * kLog2e);
-        m = vmax;
-    }
-    const float mL = fmaxf(m, -1e30f) * kLog2e;
-    float acc = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) acc += fast_exp2(__builtin_fmaf(x[j], kLog2e, -mL));
-    s += acc;
-    const uint32_t lane_floor = (uint32_t)(tl.key[K - 1] >> 32);
-    const uint32_t thr = floor_bits > lane_floor ? floor_bits : lane_floor;
-    if (order_bits(vmax) >= thr) {
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const uint64_t key = make_key(x[j], id0 + j);
-            if (key > tl.key[K - 1]) tl.insert(key);
-        }
-    }
-}
-
-// Lower bound on the k-th largest value of a row from the lanes' running maxima: the k-th
-// largest lane maximum (all copies of each round's maximum are dropped, which can only
-// lower the bound).  Returned in order_bits form; 0 when fewer than k lanes hold a value.
-// (K >= k bounds the rounds at compile time: no inner loop, which keeps the compiler's
-// load-wait placement exact in the streaming loop around it.)
+// Lower bound on the k-th largest value of a row from the lanes' maxima: the k-th largest lane
+// maximum (all copies of each round's maximum are dropped, which can only lower the bound).
+// Returned in order_bits form; 0 when fewer than k lanes hold a value.  (K >= k bounds the
+// rounds at compile time: no inner loop, which keeps the compiler's load-wait placement exact in
+// the streaming loop around it.)
 template <int K>
 __device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
     uint32_t cur = lane_max == kNegInf ? 0u : order_bits(lane_max);
@@ -162,6 +134,91 @@ __device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
         }
     }
     return best;
+}
+
+// The K best keys of a wave (descending, in every lane) from the lanes' sorted lists, by K
+// rounds of a wave-wide maximum over the list heads; the lane holding the winner drops it
+// (keys are unique: the index is part of the key).
+template <int K>
+__device__ __forceinline__ void wave_top_keys(TopList<K>& tl, uint64_t (&best)[K]) {
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+        const uint64_t head = tl.key[0];
+        uint64_t mk = head;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) mk = kmax(mk, shfl_xor64(mk, off));
+        best[r] = mk;
+        if (r + 1 < K && head == mk && mk != 0ull) {
+#pragma unroll
+            for (int j = 0; j + 1 < K; ++j) tl.key[j] = tl.key[j + 1];
+            tl.key[K - 1] = 0ull;
+        }
+    }
+}
+
+// Running state of one lane.
+template <int K>
+struct TopkLane {
+    float ref;   // reference: an element value of this lane (-inf before the first finite one)
+    float nrl;   // -ref * log2(e) (0 before the first reference)
+    float rthr;  // ref + kTopkLazyLog2 / log2(e): a larger vector maximum moves the reference
+    float s;     // sum of exp2(x log2e + nrl) over the lane's values
+    float lmax;  // largest value of the lane so far (for the wave floor)
+    float ins;   // insertion threshold: max(wave floor, the lane's K-th key) as a float
+    TopList<K> tl;
+
+    __device__ __forceinline__ void init() {
+        ref = kNegInf;
+        nrl = 0.f;
+        rthr = kNegInf;
+        s = 0.f;
+        lmax = kNegInf;
+        ins = kNegInf;
+        tl.clear();
+    }
+    __device__ __forceinline__ void refresh(uint32_t floor_bits) {
+        const uint32_t own = (uint32_t)(tl.key[K - 1] >> 32);
+        ins = threshold_of_bits(floor_bits > own ? floor_bits : own);
+    }
+};
+
+template <int NV>
+__device__ __forceinline__ float vec_max(const float (&x)[NV]) {
+    float m = x[0];
+    int j = 1;
+#pragma unroll
+    for (; j + 1 < NV; j += 2) m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, x[j]), x[j + 1]);
+#pragma unroll
+    for (; j < NV; ++j) m = __builtin_elementwise_maximum(m, x[j]);
+    return m;
+}
+
+// Absorbs NV values x (vocabulary indices id0 ..) whose maximum is vmax.  Values are never NaN
+// (an ABI precondition), so the NaN-propagating maxima above are exact.
+template <int K, int NV>
+__device__ __forceinline__ void absorb(const float (&x)[NV], float vmax, int id0, TopkLane<K>& st, uint32_t floor_bits) {
+    const bool up = vmax > st.rthr;
+    if (ballot64(up) != 0ull) {  // wave-uniform branch, rare after the first vectors
+        const float nr = -vmax * kLog2e;
+        const float f = fast_exp2(__builtin_fmaf(st.ref, kLog2e, nr));  // 0 while ref is -inf
+        st.s = up ? st.s * f : st.s;
+        st.ref = up ? vmax : st.ref;
+        st.nrl = up ? nr : st.nrl;
+        st.rthr = up ? vmax + kTopkLazyLog2 / kLog2e : st.rthr;
+    }
+    st.lmax = __builtin_elementwise_maximum(st.lmax, vmax);
+    float acc = fast_exp2(__builtin_fmaf(x[0], kLog2e, st.nrl));
+#pragma unroll
+    for (int j = 1; j < NV; ++j) acc += fast_exp2(__builtin_fmaf(x[j], kLog2e, st.nrl));
+    st.s += acc;
+    if (vmax >= st.ins) {  // rare once the floor is set
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const uint64_t key = make_key(x[j], id0 + j);
+            if (key > st.tl.key[K - 1]) st.tl.insert(key);
+        }
+        st.refresh(floor_bits);
+    }
 }
 
 // Elements of type T per 16-byte vector.
@@ -187,13 +244,15 @@ __device__ __forceinline__ void unpack(const u32x4_t& w, float (&x)[4]) {
 __device__ __forceinline__ float load_scalar(const uint16_t* p) { return bf16_bits_to_float(*p); }
 __device__ __forceinline__ float load_scalar(const float* p) { return *p; }
 
-// grid.x = rows * splits; workgroup (row, split) covers [split*chunk, min(V, (split+1)*chunk)).
-// VECTOR selects 16-byte loads (row base and chunk are then 16-byte aligned).
-template <typename T, int K, bool VECTOR>
-__global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
-    const T* __restrict__ logits, int64_t row_stride, int V, int k, int splits, int chunk,
-    float* __restrict__ conf, int32_t* __restrict__ idx, float* __restrict__ partial) {
+// grid.x = rows * splits; workgroup (row, split) covers [split * chunk, min(V, (split + 1) * chunk)).
+// VECTOR selects 16-byte loads (row base and chunk are then 16-byte aligned); without it every
+// value is a scalar load (rows of any alignment).
+template <typename T, int K, int THREADS, int U, int DEPTH, bool VECTOR>
+__global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V,
+                                                            int k, int splits, int chunk, float* __restrict__ conf,
+                                                            int32_t* __restrict__ idx, float* __restrict__ partial) {
     constexpr int NV = VecOf<T>::n;
+    constexpr int SW = THREADS * U;  // vectors per sweep of the workgroup
     const int row = blockIdx.x / splits;
     const int split = blockIdx.x - row * splits;
     const int begin = split * chunk;
@@ -201,102 +260,120 @@ __global__ __launch_bounds__(kTopkThreads) void conf_topk_kernel(
     const T* base = logits + (int64_t)row * row_stride;
     const int tid = threadIdx.x;
 
-    float m = kNegInf, s = 0.f;
-    TopList<K> tl;
-    tl.clear();
-
-    int scalar_from = begin;
+    TopkLane<K> st;
+    st.init();
     uint32_t floor_bits = 0;
+    int scalar_from = begin;
     if (VECTOR) {
         const int nvec = (end - begin) / NV;
-        const u32x4_t* vp = reinterpret_cast<const u32x4_t*>(base + begin);
-        constexpr int SW = kTopkThreads * kTopkUnroll;  // vectors per sweep of the workgroup
         const int nfull = nvec / SW;
-        int it = 0;
-        // Full sweeps: unconditional loads, the next sweep's loads in flight while the current
-        // one is absorbed (two register sets, so the loop is unrolled by two).
-        auto load_sweep = [&](int sweep, u32x4_t (&buf)[kTopkUnroll]) {
+        const u32x4_t* vp = reinterpret_cast<const u32x4_t*>(base + begin);
+        auto load = [&](int sweep, u32x4_t (&b)[U]) {
+            const int sw = sweep < nfull ? sweep : nfull - 1;  // past the end: the last sweep again
 #pragma unroll
-            for (int u = 0; u < kTopkUnroll; ++u) buf[u] = __builtin_nontemporal_load(vp + sweep * SW + u * kTopkThreads + tid);
+            for (int u = 0; u < U; ++u) b[u] = __builtin_nontemporal_load(vp + sw * SW + u * THREADS + tid);
         };
-        auto absorb_sweep = [&](int sweep, const u32x4_t (&buf)[kTopkUnroll]) {
+        auto absorb_sweep = [&](int sweep, const u32x4_t (&b)[U]) {
+            float x[U][NV];
+            float vm[U];
 #pragma unroll
-            for (int u = 0; u < kTopkUnroll; ++u) {
-                float x[NV];
-                unpack(buf[u], x);
-                absorb<K, NV>(x, begin + (sweep * SW + u * kTopkThreads + tid) * NV, m, s, tl, floor_bits);
+            for (int u = 0; u < U; ++u) {
+                unpack(b[u], x[u]);
+                vm[u] = vec_max<NV>(x[u]);
             }
-            // refresh the wave floor after sweeps 0, 1, 3, 7, 15, ...
-            if ((sweep & (sweep + 1)) == 0) floor_bits = wave_kth_floor<K>(m, k);
+#pragma unroll
+            for (int u = 0; u < U; ++u) absorb<K, NV>(x[u], vm[u], begin + (sweep * SW + u * THREADS + tid) * NV, st, floor_bits);
+            if ((sweep & (sweep + 1)) == 0) {  // after sweeps 0, 1, 3, 7, ...
+                floor_bits = wave_kth_floor<K>(st.lmax, k);
+                st.refresh(floor_bits);
+            }
         };
         if (nfull > 0) {
-            u32x4_t bufa[kTopkUnroll], bufb[kTopkUnroll];
-            load_sweep(0, bufa);
-            for (; it + 2 <= nfull; it += 2) {
-                load_sweep(it + 1, bufb);
-                __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the absorb
-                absorb_sweep(it, bufa);
-                if (it + 2 < nfull) load_sweep(it + 2, bufa);
-                __builtin_amdgcn_sched_barrier(0);
-                absorb_sweep(it + 1, bufb);
-            }
-            if (it < nfull) {  // odd count: the last full sweep is already loaded in bufa
-                absorb_sweep(it, bufa);
-                ++it;
-            }
-        }
-        // Last, partial sweep: per-vector bounds.
-        for (int vb = nfull * SW; vb < nvec; vb += SW, ++it) {
-            u32x4_t buf[kTopkUnroll];
+            u32x4_t buf[DEPTH][U];
 #pragma unroll
-            for (int u = 0; u < kTopkUnroll; ++u) {
-                const int vi = vb + u * kTopkThreads + tid;
-                if (vi < nvec) buf[u] = __builtin_nontemporal_load(vp + vi);
-            }
+            for (int d = 0; d + 1 < DEPTH; ++d) load(d, buf[d]);
+            {  // a first floor from sweep 0's lane maxima, so that sweep 0 already inserts rarely
+                float lm = kNegInf;
 #pragma unroll
-            for (int u = 0; u < kTopkUnroll; ++u) {
-                const int vi = vb + u * kTopkThreads + tid;
-                if (vi < nvec) {
-                    float x[NV];
-                    unpack(buf[u], x);
-                    absorb<K, NV>(x, begin + vi * NV, m, s, tl, floor_bits);
+                for (int u = 0; u < U; ++u) {
+                    float x0[NV];
+                    unpack(buf[0][u], x0);
+                    lm = __builtin_elementwise_maximum(lm, vec_max<NV>(x0));
+                }
+                floor_bits = wave_kth_floor<K>(lm, k);
+                st.refresh(floor_bits);
+            }
+            int it = 0;
+            for (; it + DEPTH <= nfull; it += DEPTH) {
+#pragma unroll
+                for (int j = 0; j < DEPTH; ++j) {
+                    load(it + j + DEPTH - 1, buf[(j + DEPTH - 1) % DEPTH]);
+                    __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the absorb
+                    absorb_sweep(it + j, buf[j]);
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            if ((it & (it + 1)) == 0) floor_bits = wave_kth_floor<K>(m, k);
+            // the remaining nfull - it < DEPTH sweeps are already in buf[0 ..]
+#pragma unroll
+            for (int j = 0; j + 1 < DEPTH; ++j)
+                if (it + j < nfull) absorb_sweep(it + j, buf[j]);
+        }
+        // last, partial sweep: one vector at a time
+        for (int v = nfull * SW + tid; v < nvec; v += THREADS) {
+            float x[NV];
+            unpack(__builtin_nontemporal_load(vp + v), x);
+            absorb<K, NV>(x, vec_max<NV>(x), begin + v * NV, st, floor_bits);
         }
         scalar_from = begin + nvec * NV;
     }
-    for (int e = scalar_from + tid; e < end; e += kTopkThreads) {
-        float x[1] = {load_scalar(base + e)};
-        absorb<K, 1>(x, e, m, s, tl, floor_bits);
+    for (int e = scalar_from + tid; e < end; e += THREADS) {
+        const float x[1] = {load_scalar(base + e)};
+        absorb<K, 1>(x, x[0], e, st, floor_bits);
     }
 
-    // lanes -> wave
-    wave_merge<K>(m, s, tl);
+    // lanes -> wave: (reference, sum) by shuffles, the keys by K rounds of a wave maximum
+    float m = st.ref, s = st.s;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
+    uint64_t best[K];
+    wave_top_keys<K>(st.tl, best);
     // waves -> workgroup
-    constexpr int NW = kTopkThreads / 64;
-    __shared__ float sh_m[NW], sh_s[NW];
-    __shared__ uint64_t sh_k[NW][K];
-    const int lane = tid & 63, wave = tid >> 6;
-    if (lane == 0) {
-        sh_m[wave] = m;
-        sh_s[wave] = s;
+    constexpr int NW = THREADS / 64;
+    TopList<K> tl;
 #pragma unroll
-        for (int j = 0; j < K; ++j) sh_k[wave][j] = tl.key[j];
-    }
-    __syncthreads();
-    if (wave != 0) return;
-    if (lane < NW) {
-        m = sh_m[lane];
-        s = sh_s[lane];
+    for (int j = 0; j < K; ++j) tl.key[j] = best[j];
+    const int lane = tid & 63;
+    if (NW > 1) {
+        __shared__ float sh_m[NW], sh_s[NW];
+        __shared__ uint64_t sh_k[NW][K];
+        const int wave = tid >> 6;
+        if (lane == 0) {
+            sh_m[wave] = m;
+            sh_s[wave] = s;
 #pragma unroll
-        for (int j = 0; j < K; ++j) tl.key[j] = sh_k[lane][j];
-    } else {
-        m = kNegInf;
-        s = 0.f;
-        tl.clear();
+            for (int j = 0; j < K; ++j) sh_k[wave][j] = best[j];
+        }
+        __syncthreads();
+        if (wave != 0) return;
+        if (lane < NW) {
+            m = sh_m[lane];
+            s = sh_s[lane];
+#pragma unroll
+            for (int j = 0; j < K; ++j) tl.key[j] = sh_k[lane][j];
+        } else {
+            m = kNegInf;
+            s = 0.f;
+            tl.clear();
+        }
+#pragma unroll
+        for (int off = NW / 2; off >= 1; off >>= 1) {
+            merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
+            uint64_t o[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) o[j] = shfl_xor64(tl.key[j], off);
+            tl.merge(o);
+        }
     }
-    wave_merge<K>(m, s, tl);
     if (lane != 0) return;
     if (partial != nullptr) {
         float* rec = partial + ((int64_t)row * splits + split) * kTopkRecord;
@@ -337,41 +414,48 @@ __global__ __launch_bounds__(64) void conf_topk_merge_kernel(const float* __rest
         for (int j = 0; j < K; ++j) o[j] = rk[j];
         tl.merge(o);
     }
-    wave_merge<K>(m, s, tl);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
+    uint64_t best[K];
+    wave_top_keys<K>(tl, best);
     if (lane != 0) return;
     const float inv = 1.0f / s;
 #pragma unroll
     for (int j = 0; j < K; ++j) {
         if (j < k) {
-            conf[(int64_t)row * k + j] = fast_exp2((key_value(tl.key[j]) - m) * kLog2e) * inv;
-            idx[(int64_t)row * k + j] = key_index(tl.key[j]);
+            conf[(int64_t)row * k + j] = fast_exp2((key_value(best[j]) - m) * kLog2e) * inv;
+            idx[(int64_t)row * k + j] = key_index(best[j]);
         }
     }
 }
 
+// Launch shape of the pass.  threads: lanes per row slice; unroll / depth: the register ring
+// (vectors per sweep, sweeps held); splits / chunk: slices per row and their length.
 struct TopkPlan {
-    int splits;
-    int chunk;
+    int threads, unroll, depth;
+    int splits, chunk;
 };
 
-// Splits short batches so that at least ~512 workgroups stream the rows.  More, shorter
-// slices cost more than they gain: each slice pays a workgroup reduction and a partial record,
-// and the merge kernel grows with them (measured on 256-1024-row batches: a 2048 target was
-// 15-25% slower than 512).
+// Measured on the 8B shapes (vocab 126464-152064, bf16): with many rows one wave per row and a
+// 3-sweep ring of 2 vectors streams fastest (32768 rows: 6.7 TB/s); 1024 rows run best with
+// 2 waves per row and 8-vector sweeps (2 waves per SIMD), 256 rows with 8 waves per row.  Fewer
+// rows than that also split each row, so that the launch keeps about 128 workgroups.
 inline TopkPlan plan_conf_topk(int64_t rows, int64_t vocab, int vec) {
-    TopkPlan p{1, (int)vocab};
-    const int64_t target = 512;
+    TopkPlan p{64, 2, 3, 1, (int)vocab};
+    if (rows >= 4096) return p;
+    if (rows >= 512) return TopkPlan{128, 8, 2, 1, (int)vocab};
+    p = TopkPlan{512, 2, 2, 1, (int)vocab};
+    const int64_t target = 128;
     if (rows <= 0 || rows >= target) return p;
-    const int64_t align = (int64_t)kTopkThreads * vec;  // one full sweep of the workgroup
-    int64_t want = (target + rows - 1) / rows;
-    int64_t max_by_len = (vocab + 4 * align - 1) / (4 * align);  // >= 4 sweeps per slice
+    const int64_t align = (int64_t)p.threads * vec;  // one vector per lane
+    const int64_t want = (target + rows - 1) / rows;
+    const int64_t max_by_len = (vocab + 4 * align - 1) / (4 * align);  // >= 4 vectors per lane and slice
     int64_t splits = want < max_by_len ? want : max_by_len;
     if (splits > 64) splits = 64;
     if (splits <= 1) return p;
     int64_t chunk = (vocab + splits - 1) / splits;
     chunk = (chunk + align - 1) / align * align;
-    splits = (vocab + chunk - 1) / chunk;
-    p.splits = (int)splits;
+    p.splits = (int)((vocab + chunk - 1) / chunk);
     p.chunk = (int)chunk;
     return p;
 }

@@ -62,24 +62,37 @@ traj_status check_logits(const traj_logits_shape* sh, int32_t k) {
     return TRAJ_OK;
 }
 
+template <typename T, int K, int THREADS, int U, int DEPTH, bool VECTOR>
+void launch_conf_kernel(const T* lg, const traj_logits_shape* sh, int k, const TopkPlan& plan, float* conf,
+                        int32_t* idx, float* partial, hipStream_t st) {
+    const dim3 grid((unsigned)(sh->rows * plan.splits));
+    hipLaunchKernelGGL((conf_topk_kernel<T, K, THREADS, U, DEPTH, VECTOR>), grid, dim3(THREADS), 0, st, lg,
+                       sh->row_stride, (int)sh->vocab, k, plan.splits, plan.chunk, conf, idx, partial);
+}
+
+// The plan's split records go to `ws` (at least traj_confidence_topk_workspace_size() bytes);
+// without one the rows run unsplit.
 template <typename T, int K>
 traj_status launch_topk_k(const void* logits, const traj_logits_shape* sh, int k, float* conf, int32_t* idx,
                           void* ws, size_t ws_bytes, hipStream_t st) {
-    const int vec = VecOf<T>::n;
     const bool vector_ok = aligned16(logits) && ((sh->row_stride * (int64_t)sizeof(T)) % 16 == 0);
-    TopkPlan plan = plan_conf_topk(sh->rows, sh->vocab, vec);
+    TopkPlan plan = plan_conf_topk(sh->rows, sh->vocab, VecOf<T>::n);
     const size_t need = (size_t)sh->rows * plan.splits * kTopkRecord * sizeof(float);
-    if (plan.splits > 1 && (ws == nullptr || ws_bytes < need || !aligned16(ws))) plan = TopkPlan{1, (int)sh->vocab};
+    if (plan.splits > 1 && (ws == nullptr || ws_bytes < need || !aligned16(ws))) {
+        plan.splits = 1;
+        plan.chunk = (int)sh->vocab;
+    }
     if (sh->rows == 0) return TRAJ_OK;
-    const int grid = (int)(sh->rows * plan.splits);
     float* partial = plan.splits > 1 ? static_cast<float*>(ws) : nullptr;
     const T* lg = static_cast<const T*>(logits);
-    if (vector_ok) {
-        hipLaunchKernelGGL((conf_topk_kernel<T, K, true>), dim3(grid), dim3(kTopkThreads), 0, st, lg,
-                           sh->row_stride, (int)sh->vocab, k, plan.splits, plan.chunk, conf, idx, partial);
+    if (!vector_ok) {
+        launch_conf_kernel<T, K, 256, 1, 1, false>(lg, sh, k, plan, conf, idx, partial, st);
+    } else if (plan.threads == 64) {
+        launch_conf_kernel<T, K, 64, 2, 3, true>(lg, sh, k, plan, conf, idx, partial, st);
+    } else if (plan.threads == 128) {
+        launch_conf_kernel<T, K, 128, 8, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     } else {
-        hipLaunchKernelGGL((conf_topk_kernel<T, K, false>), dim3(grid), dim3(kTopkThreads), 0, st, lg,
-                           sh->row_stride, (int)sh->vocab, k, plan.splits, plan.chunk, conf, idx, partial);
+        launch_conf_kernel<T, K, 512, 2, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     }
     if (plan.splits > 1) {
         hipLaunchKernelGGL((conf_topk_merge_kernel<K>), dim3((unsigned)sh->rows), dim3(64), 0, st, partial,

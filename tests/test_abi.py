@@ -88,12 +88,14 @@ def test_logits_argument_errors():
     assert call(good, 0) == 7 and call(good, 9) == 7                  # k range
     assert call(_lib.LogitsShape(4, 2, 2, 1), 3) == 7                 # k > vocab
     assert call(good, 3, logits=None) == 1
-    need = lib.traj_confidence_topk_workspace_size(ctypes.byref(good), 3)
+    few = _lib.LogitsShape(40, 126464, 126464, 0)                    # a short batch: rows are split
+    need = lib.traj_confidence_topk_workspace_size(ctypes.byref(few), 3)
     assert need > 0
-    assert call(good, 3, ws=FAKE, ws_bytes=need - 1) == 5             # too small
-    assert call(good, 3, ws=ctypes.c_void_p(0x1004), ws_bytes=need) == 5  # misaligned
-    big = _lib.LogitsShape(32768, 126464, 126464, 0)
-    assert lib.traj_confidence_topk_workspace_size(ctypes.byref(big), 3) == 0
+    assert call(few, 3, ws=FAKE, ws_bytes=need - 1) == 5              # too small
+    assert call(few, 3, ws=ctypes.c_void_p(0x1004), ws_bytes=need) == 5  # misaligned
+    for rows in (256, 1024, 32768):                                   # enough rows: never split
+        big = _lib.LogitsShape(rows, 126464, 126464, 0)
+        assert lib.traj_confidence_topk_workspace_size(ctypes.byref(big), 3) == 0
 
 
 @needs_lib

@@ -38,12 +38,21 @@ def test_tiny_fp32_full():
 
 
 def test_8b_siblings_full_size():
-    """256 rows x 126464 bf16 -- the launch splits rows (short batch path)."""
+    """256 rows x 126464 bf16 -- the short-batch launch (8 waves per row), every row checked."""
     wl = WORKLOADS[2]
     d = decode_inputs(wl, seed_for(2))
     lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(2)).cuda()
-    assert tsp.confidence_topk_workspace_size(lg, 3) > 0
     _check(lg, 3, label="8b-siblings")
+
+
+@pytest.mark.parametrize("rows", [1, 5, 40, 127])
+def test_split_rows_full_vocab(rows):
+    """Fewer than 128 rows: each row is split across workgroups and the partial records merged."""
+    wl = WORKLOADS[2]
+    d = decode_inputs(wl, seed_for(2, 1))
+    lg = make_logits(d["row_margin"][:rows], d["row_top"][:rows], wl.V, torch.bfloat16, seed_for(2, 1)).cuda()
+    assert tsp.confidence_topk_workspace_size(lg, 3) > 0
+    _check(lg, 3, label=f"split rows={rows}")
 
 
 @pytest.mark.parametrize("cid", [3, 4])
