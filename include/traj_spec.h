@@ -169,6 +169,20 @@ traj_status traj_confidence_topk(const void* logits, int32_t k, float* conf, int
                                  const traj_logits_shape* shape,
                                  void* workspace, size_t workspace_bytes, void* stream);
 
+/* traj_confidence_topk for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same kernels and results
+ * bit for bit, with the split records of short batches in a fixed scratch array of
+ * TRAJ_TOPK_SCRATCH_BYTES that the library holds on each device it runs on until the process
+ * ends (its address is looked up on the first call on a device).  Calls no allocating routine.
+ * Every call on one device shares that array: calls whose executions overlap on one device
+ * (e.g. on two streams) race; calls ordered on one stream do not (nothing in the array needs to
+ * start at zero).  A shape whose split records would exceed the array returns TRAJ_E_WORKSPACE
+ * (no shape the current plan splits needs more than about 19 KB).  Other arguments, limits and
+ * errors as traj_confidence_topk. */
+#define TRAJ_TOPK_SCRATCH_BYTES 65536
+traj_status traj_confidence_topk_noalloc(const void* logits, int32_t k, float* conf, int32_t* idx,
+                                         const traj_logits_shape* shape, void* stream);
+
 /* ------------------------------------------------------------------------------------
  * 3. Acceptance  (Sec. 3.3 "Verification procedure"; Sec. 2.1 threshold decoding;
  *    Sec. 3.1 logit reuse; Alg. 1 phase 1)

@@ -40,6 +40,7 @@ from ._lib import (  # noqa: F401
     built_digest,
     check_build,
     confidence_topk,
+    confidence_topk_noalloc,
     confidence_topk_workspace_size,
     device_status,
     interblock_trigger,

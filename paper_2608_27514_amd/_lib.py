@@ -84,6 +84,8 @@ EXPORTS = {
     "traj_confidence_topk": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.POINTER(LogitsShape), ctypes.c_void_p, ctypes.c_size_t,
                                               ctypes.c_void_p]),
+    "traj_confidence_topk_noalloc": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                                      ctypes.c_void_p, ctypes.POINTER(LogitsShape), ctypes.c_void_p]),
     "traj_accept": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Drafts), ctypes.c_float,
                                      ctypes.POINTER(Accepted), ctypes.c_void_p]),
     "traj_verify_attn_peers": (ctypes.c_int32, [ctypes.c_void_p] * 8 + [ctypes.POINTER(AttnShape), ctypes.c_void_p,
@@ -300,6 +302,27 @@ def confidence_topk(logits, k, conf=None, idx=None, workspace=None, stream=None)
     st = _lib().traj_confidence_topk(ctypes.c_void_p(logits.data_ptr()), int(k), _ptr(conf), _ptr(idx),
                                      ctypes.byref(shape), _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "traj_confidence_topk")
+    return conf, idx
+
+
+def confidence_topk_noalloc(logits, k, conf=None, idx=None, stream=None):
+    """traj_confidence_topk_noalloc: the same results as :func:`confidence_topk` without a
+    workspace (the library's fixed per-device scratch holds the split records)."""
+    if not isinstance(logits, torch.Tensor) or not logits.is_cuda:
+        raise TypeError("logits must be a CUDA (HIP) tensor")
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be 2-D with a contiguous last dimension")
+    shape = logits_shape(logits)
+    R = logits.shape[0]
+    if conf is None:
+        conf = torch.empty((R, k), dtype=torch.float32, device=logits.device)
+    if idx is None:
+        idx = torch.empty((R, k), dtype=torch.int32, device=logits.device)
+    _dev(conf, "conf", torch.float32)
+    _dev(idx, "idx", torch.int32)
+    st = _lib().traj_confidence_topk_noalloc(ctypes.c_void_p(logits.data_ptr()), int(k), _ptr(conf), _ptr(idx),
+                                             ctypes.byref(shape), _stream(stream))
+    _check(st, "traj_confidence_topk_noalloc")
     return conf, idx
 
 

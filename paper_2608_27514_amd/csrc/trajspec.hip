@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstdint>
+#include <mutex>
 
 #include "../../include/traj_spec.h"
 #include "accept.hpp"
@@ -17,9 +18,32 @@
 #include "tree.hpp"
 #include "verify_attn.hpp"
 
+// Fixed device scratch of traj_confidence_topk_noalloc: the split records of short batches
+// (at most TRAJ_TOPK_SCRATCH_BYTES).  Host code must not pass this name to a kernel or a copy: on
+// the host it is only a handle; the device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) unsigned char scratch[TRAJ_TOPK_SCRATCH_BYTES];
+
 namespace {
 
 using namespace trajspec;
+
+// Device address of `scratch` on the current device, looked up once per device.
+constexpr int kScratchMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kScratchMaxDevices];
+
+traj_status device_scratch(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchMaxDevices) return TRAJ_E_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return TRAJ_E_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return TRAJ_OK;
+}
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
@@ -410,6 +434,22 @@ traj_status traj_confidence_topk(const void* logits, int32_t k, float* conf, int
     hipStream_t s = as_stream(stream);
     if (shape->dtype == TRAJ_BF16) return launch_topk<uint16_t>(logits, shape, k, conf, idx, workspace, workspace_bytes, s);
     return launch_topk<float>(logits, shape, k, conf, idx, workspace, workspace_bytes, s);
+}
+
+traj_status traj_confidence_topk_noalloc(const void* logits, int32_t k, float* conf, int32_t* idx,
+                                         const traj_logits_shape* shape, void* stream) {
+    if (shape == nullptr) return TRAJ_E_NULL;
+    traj_status st = check_logits(shape, k);
+    if (st != TRAJ_OK) return st;
+    if (shape->rows == 0) return TRAJ_OK;
+    if (logits == nullptr || conf == nullptr || idx == nullptr) return TRAJ_E_NULL;
+    const size_t need = traj_confidence_topk_workspace_size(shape, k);
+    if (need > (size_t)TRAJ_TOPK_SCRATCH_BYTES) return TRAJ_E_WORKSPACE;  // split records beyond the fixed scratch
+    void* ws = nullptr;
+    if (need > 0 && (st = device_scratch(&ws)) != TRAJ_OK) return st;
+    hipStream_t s = as_stream(stream);
+    if (shape->dtype == TRAJ_BF16) return launch_topk<uint16_t>(logits, shape, k, conf, idx, ws, need, s);
+    return launch_topk<float>(logits, shape, k, conf, idx, ws, need, s);
 }
 
 traj_status traj_accept(const float* conf, const int32_t* idx, const traj_drafts* drafts, float threshold,

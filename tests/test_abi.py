@@ -99,6 +99,30 @@ def test_logits_argument_errors():
 
 
 @needs_lib
+def test_noalloc_logit_pass_arguments_and_scratch_bound():
+    lib = _lib.load()
+
+    def call(shape, k, logits=FAKE):
+        return lib.traj_confidence_topk_noalloc(logits, k, FAKE, FAKE, ctypes.byref(shape), None)
+
+    assert call(_lib.LogitsShape(4, 100, 100, 9), 3) == 3
+    assert call(_lib.LogitsShape(4, 100, 99, 0), 3) == 2
+    assert call(_lib.LogitsShape(4, 100, 100, 0), 9) == 7
+    assert call(_lib.LogitsShape(4, 100, 100, 0), 3, logits=None) == 1
+    assert call(_lib.LogitsShape(0, 100, 100, 0), 3, logits=None) == 0  # no rows: nothing to do
+    assert lib.traj_confidence_topk_noalloc(FAKE, 3, FAKE, FAKE, None, None) == 1
+    # every shape the plan splits fits the fixed scratch (so the entry point never refuses one)
+    limit = int(re.search(r"#define TRAJ_TOPK_SCRATCH_BYTES (\d+)", open(HEADER).read()).group(1))
+    worst = 0
+    for dtype in (0, 1):
+        for rows in range(1, 600):
+            for vocab in (1000, 32000, 126464, 152064, 262144, (1 << 31) - 1):
+                sh = _lib.LogitsShape(rows, vocab, vocab, dtype)
+                worst = max(worst, lib.traj_confidence_topk_workspace_size(ctypes.byref(sh), 8))
+    assert 0 < worst <= limit, worst
+
+
+@needs_lib
 def test_accept_argument_errors():
     lib = _lib.load()
     f = 0x1000
