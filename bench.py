@@ -362,16 +362,46 @@ def step_record(wl, x, ms_step, kernels, n_copies, steps):
     }
 
 
+def time_kernels_apart(copies, buf, tau, stream, reps):
+    """Each kernel of the step on its own: `reps` back-to-back launches over the rotated copies
+    between two HIP events (the per-call event pairs of the step timing add their own overhead,
+    which matters for kernels of tens of microseconds).  Returns per-launch ms."""
+    n = len(copies)
+    calls = {
+        "verify_attn": lambda x: tsp.verify_attn(x.q, x.kc, x.vc, x.kd, x.vd, x.parent, out=buf.out, stream=stream),
+        "confidence_topk": lambda x: tsp.confidence_topk(x.logits, x.wl.k, conf=buf.conf, idx=buf.idx,
+                                                         workspace=buf.ws, stream=stream),
+        "accept": lambda x: tsp.accept(buf.conf, buf.idx, x.tokens, x.parent, x.committed, x.conf0, x.idx0, tau,
+                                       out=buf.acc, stream=stream),
+    }
+    out = {}
+    for name, fn in calls.items():
+        for i in range(3):
+            fn(copies[i % n])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(reps):
+            fn(copies[i % n])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = e0.elapsed_time(e1) / reps
+    return out
+
+
 def time_config(cid, stream, steps, warmup):
-    """A workload other than the headline one, timed in the same run exactly as the headline step
-    (rotated copies, per-kernel HIP events on the launch stream)."""
+    """A workload other than the headline one, timed in the same run: the step exactly as the
+    headline step (rotated copies, HIP events on the launch stream around every call), and each
+    kernel in back-to-back launches of its own (the fractions of the roofline use these)."""
     wl = WORKLOADS[cid]
     dev = torch.device("cuda:0")
     copies = make_copies(wl, wl.tau, dev)
     buf = Buffers(wl, dev, copies[0].logits)
     torch.cuda.synchronize()
-    ms_step, kernels = time_steps(copies, buf, wl.tau, stream, steps, warmup)
+    ms_step, in_step = time_steps(copies, buf, wl.tau, stream, steps, warmup)
+    kernels = time_kernels_apart(copies, buf, wl.tau, stream, steps)
     rec = step_record(wl, copies[0], ms_step, kernels, len(copies), steps)
+    rec["kernel_us_in_step"] = {k: v * 1e3 for k, v in in_step.items()}
     run_step(copies[0], buf, wl.tau, stream)
     torch.cuda.synchronize()
     rec["accepted_tokens_per_step"] = float(buf.acc["n_accepted"].sum().item())
