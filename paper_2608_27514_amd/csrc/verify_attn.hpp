@@ -306,24 +306,47 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t krs, __amdgpu_b
     cache_rows_dma<D, RAGGED, true>(vrs, kv_stride, t * kAttnTile, S, wave, ln, stage + G::kTileElems);
 }
 
-// Softmax phase of a 64-key step: the scores of two blocks (s[0], s[1]) against the query's
-// reference, after folding their joint maximum into it; pf[b][half] receives the bf16 weights
-// of block b, keys 16 half .. 16 half + 15, in MFMA B-operand order.
+// Softmax phase of a 64-key step: the weights of two blocks (s[0], s[1]) against the query's
+// reference; pf[b][half] receives the bf16 weights of block b, keys 16 half .. 16 half + 15, in MFMA
+// B-operand order.  A weight exceeds 2^kLazyLog2 exactly when its score passes the lazy trigger, so
+// the lane's weight sum of the step is compared with that bound instead of taking the block maximum
+// first: only then (or while the reference is still -inf) does the wave take the path that folds the
+// true joint maximum in and recomputes.  The reference therefore moves at the same scores as with a
+// maximum taken every step (up to the rounding of the two tests at the trigger itself); on every
+// workload measured the outputs are the same bits.  Saves 16 three-input maxima, a lane swap and a
+// compare per step of each wave.
 template <int D>
 __device__ __forceinline__ void softmax_phase(const f32x16_t (&s)[2], float c, float thr, SoftState& st,
                                               f32x16_t (&o)[D / 32], bf16x8_t (&pf)[2][2]) {
-    const float mx = max16(s[1], max16(s[0], kNegInf));
-    fold_max<D>(pair_max(mx), c, thr, st, o);
-    const float neg_mc = st.neg_mc;
+    float neg_mc = st.neg_mc;
     float sum0 = 0.f, sum1 = 0.f;
+    float p0[16], p1[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        const float p0 = fast_exp2(__builtin_fmaf(s[0][v], c, neg_mc));
-        const float p1 = fast_exp2(__builtin_fmaf(s[1][v], c, neg_mc));
-        sum0 += p0;
-        sum1 += p1;
-        pf[0][v >> 3][v & 7] = (__bf16)p0;
-        pf[1][v >> 3][v & 7] = (__bf16)p1;
+        p0[v] = fast_exp2(__builtin_fmaf(s[0][v], c, neg_mc));
+        p1[v] = fast_exp2(__builtin_fmaf(s[1][v], c, neg_mc));
+        sum0 += p0[v];
+        sum1 += p1[v];
+    }
+    const bool big = !(sum0 + sum1 <= (float)(1 << (int)kLazyLog2)) || st.m == kNegInf;
+    if (ballot64(big) != 0ull) {
+        const float mx = max16(s[1], max16(s[0], kNegInf));
+        fold_max<D>(pair_max(mx), c, thr, st, o);
+        neg_mc = st.neg_mc;
+        sum0 = 0.f;
+        sum1 = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            p0[v] = fast_exp2(__builtin_fmaf(s[0][v], c, neg_mc));
+            p1[v] = fast_exp2(__builtin_fmaf(s[1][v], c, neg_mc));
+            sum0 += p0[v];
+            sum1 += p1[v];
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        pf[0][v >> 3][v & 7] = (__bf16)p0[v];
+        pf[1][v >> 3][v & 7] = (__bf16)p1[v];
     }
     st.lsum += sum0 + sum1;
 }
