@@ -362,6 +362,52 @@ def step_record(wl, x, ms_step, kernels, n_copies, steps):
     }
 
 
+FLOOR_LIB = os.path.join(ROOT, "paper_2608_27514_amd", "libtrajfloor.so")
+
+
+def logit_floor(copies, stream, reps):
+    """The logit pass's streaming-read floor on the same logit rows: libtrajfloor's read-only kernel
+    with the launch shape the pass plans for this shape (workgroup size, load ring, row slices),
+    `reps` back-to-back launches over the rotated copies between two HIP events.  None when the
+    library is not built or the rows are not on the pass's 16-byte vector path."""
+    import ctypes
+    if not os.path.exists(FLOOR_LIB):
+        return None
+    lib = ctypes.CDLL(FLOOR_LIB)
+    fn = lib.traj_floor_logit_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p]
+    lg0 = copies[0].logits
+    wl = copies[0].wl
+    sink = torch.zeros(4096, dtype=torch.int32, device=lg0.device)
+    shape = (ctypes.c_int32 * 4)()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+
+    def call(x):
+        lg = x.logits
+        return fn(ctypes.c_void_p(lg.data_ptr()), lg.shape[0], lg.shape[1], lg.stride(0), lg.element_size(),
+                  ctypes.c_void_p(sink.data_ptr()), shape, sp)
+
+    n = len(copies)
+    if call(copies[0]) != 0:
+        return None
+    for i in range(3):
+        call(copies[i % n])
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(reps):
+        call(copies[i % n])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gbs = logit_bytes(wl) / (ms * 1e-3) / 1e9
+    return {"kernel": "read-only floor (libtrajfloor), same launch shape and loads as the pass",
+            "launch": {"threads": shape[0], "unroll": shape[1], "depth": shape[2], "row_slices": shape[3]},
+            "us": ms * 1e3, "gbs": gbs, "frac_of_hbm": gbs / PEAK_HBM_GBS}
+
+
 def time_kernels_apart(copies, buf, tau, stream, reps):
     """Each kernel of the step on its own: `reps` back-to-back launches over the rotated copies
     between two HIP events (the per-call event pairs of the step timing add their own overhead,
@@ -402,6 +448,10 @@ def time_config(cid, stream, steps, warmup):
     kernels = time_kernels_apart(copies, buf, wl.tau, stream, steps)
     rec = step_record(wl, copies[0], ms_step, kernels, len(copies), steps)
     rec["kernel_us_in_step"] = {k: v * 1e3 for k, v in in_step.items()}
+    fl = logit_floor(copies, stream, steps)
+    if fl is not None:
+        fl["logit_pass_over_floor"] = kernels["confidence_topk"] * 1e3 / fl["us"]
+    rec["logit_pass"]["floor"] = fl
     run_step(copies[0], buf, wl.tau, stream)
     torch.cuda.synchronize()
     rec["accepted_tokens_per_step"] = float(buf.acc["n_accepted"].sum().item())
@@ -716,6 +766,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the measurements beside the step (warm cache, tree build, inter-block), e.g. "
                          "for a kernel trace of the step alone")
+    ap.add_argument("--with-floor", action="store_true",
+                    help="time the logit pass's streaming-read floor even with --no-extras")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip timing the other workloads (the 'configs' record)")
     ap.add_argument("--config-steps", type=int, default=50, help="timed steps of each other workload")
@@ -787,6 +839,9 @@ def main():
             if cid != wl.cid:
                 log(f"config {WORKLOADS[cid].name}")
                 configs[WORKLOADS[cid].name] = time_config(cid, stream, args.config_steps, args.warmup)
+    floor = logit_floor(copies, stream, args.steps) if (args.with_floor or not args.no_extras) else None
+    if floor is not None:
+        floor["logit_pass_over_floor"] = t_conf * 1e3 / floor["us"]
     status = tsp.device_status(reset=True)
 
     result = {
@@ -821,7 +876,7 @@ def main():
         "kernels_ms": {"verify_attn": t_attn, "confidence_topk": t_conf, "accept": t_acc},
         "logit_pass": {"bound": "hbm", "achieved": l_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                        "frac": l_gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": logit_bytes(wl),
-                       "traffic": measured_traffic("confidence_topk", wl.name)},
+                       "traffic": measured_traffic("confidence_topk", wl.name), "floor": floor},
         "attention_hbm_bytes_per_launch": attn_bytes(wl),
         "accepted_tokens_per_step": {str(tau): float(acc_main.sum())},
         "mean_accepted_per_sequence": {str(tau): float(acc_main.mean())},

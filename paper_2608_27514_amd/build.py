@@ -13,6 +13,8 @@ ROOT = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 LIB_NAME = "libtrajspec.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
+# measurement aid: the streaming-read floor of the logit pass (not part of the C ABI)
+FLOOR_PATH = os.path.join(PKG_DIR, "libtrajfloor.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -45,8 +47,8 @@ def source_digest():
     a loaded binary can be checked against the checked-out sources."""
     import hashlib
     h = hashlib.sha256()
-    files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC))
-             if f.endswith((".hip", ".hpp", ".h"))]
+    files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith((".hpp", ".h"))]
+    files += sources()
     files.append(os.path.join(ROOT, "include", "traj_spec.h"))
     for path in files:
         h.update(os.path.relpath(path, ROOT).encode() + b"\0")
@@ -73,7 +75,22 @@ def build(verbose=False, extra_flags=()):
     if verbose and out.strip():
         print(out, flush=True)
     os.replace(tmp, LIB_PATH)
+    build_floor(verbose)
     return LIB_PATH
+
+
+def build_floor(verbose=False):
+    """Compile libtrajfloor.so, the logit pass's streaming-read floor (a measurement aid)."""
+    tmp = FLOOR_PATH + ".tmp"
+    cmd = [hipcc_path(), *HIPCC_FLAGS, "-I", CSRC, os.path.join(CSRC, "stream_floor.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        out = "\n".join(line for line in (res.stdout + res.stderr).splitlines() if "packed-fp32-ops" not in line)
+        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
+    os.replace(tmp, FLOOR_PATH)
+    return FLOOR_PATH
 
 
 if __name__ == "__main__":

@@ -261,3 +261,24 @@ def test_layer_and_linear_argument_errors():
     assert call(weights=_lib.LayerWeights(*([0x1000] * 5 + [0]))) == 1
     assert call(weights=_lib.LayerWeights(*([0x1000] * 5 + [0x1008]))) == 2
     assert call(ws_bytes=16) == 5
+
+
+FLOOR_LIB = os.path.join(ROOT, "paper_2608_27514_amd", "libtrajfloor.so")
+
+
+@pytest.mark.skipif(not os.path.exists(FLOOR_LIB), reason="libtrajfloor.so not built")
+def test_floor_library_rejects_shapes_off_the_vector_path():
+    """The logit pass's read-only floor (a measurement aid) refuses what the pass's vector path
+    would not take, before any launch."""
+    lib = ctypes.CDLL(FLOOR_LIB)
+    fn = lib.traj_floor_logit_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p]
+    sink = FAKE
+    assert fn(None, 4, 1024, 1024, 2, sink, None, None) == -1            # no data
+    assert fn(FAKE, 4, 1024, 1024, 2, None, None, None) == -1            # no sink
+    assert fn(FAKE, 4, 1001, 1001, 2, sink, None, None) == -1            # rows not whole 16-byte vectors
+    assert fn(ctypes.c_void_p(0x1002), 4, 1024, 1024, 2, sink, None, None) == -1  # misaligned
+    assert fn(FAKE, 4, 1024, 1000, 2, sink, None, None) == -1            # stride < vocab
+    assert fn(FAKE, 4, 1024, 1024, 3, sink, None, None) == -1            # element size
