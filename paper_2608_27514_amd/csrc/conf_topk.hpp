@@ -214,8 +214,13 @@ __device__ __forceinline__ void absorb(const float (&x)[NV], float vmax, int id0
     if (vmax >= st.ins) {  // rare once the floor is set
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-            const uint64_t key = make_key(x[j], id0 + j);
-            if (key > st.tl.key[K - 1]) st.tl.insert(key);
+            // A value below the threshold is below the row's k-th largest (the wave floor) or below
+            // the lane's own K-th key: it can change neither the result nor the list, so it skips
+            // the key and the insertion network (a branch per value, taken by few lanes).
+            if (x[j] >= st.ins) {
+                const uint64_t key = make_key(x[j], id0 + j);
+                if (key > st.tl.key[K - 1]) st.tl.insert(key);
+            }
         }
         st.refresh(floor_bits);
     }
