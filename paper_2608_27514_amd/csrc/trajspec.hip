@@ -113,8 +113,10 @@ traj_status launch_topk_k(const void* logits, const traj_logits_shape* sh, int k
         launch_conf_kernel<T, K, 256, 1, 1, false>(lg, sh, k, plan, conf, idx, partial, st);
     } else if (plan.threads == 64) {
         launch_conf_kernel<T, K, 64, 2, 3, true>(lg, sh, k, plan, conf, idx, partial, st);
-    } else if (plan.threads == 128) {
-        launch_conf_kernel<T, K, 128, 8, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
+    } else if (plan.threads == 256) {
+        launch_conf_kernel<T, K, 256, 4, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
+    } else if (plan.threads == 1024) {
+        launch_conf_kernel<T, K, 1024, 4, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     } else {
         launch_conf_kernel<T, K, 512, 2, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     }

@@ -38,7 +38,7 @@ def test_tiny_fp32_full():
 
 
 def test_8b_siblings_full_size():
-    """256 rows x 126464 bf16 -- the short-batch launch (8 waves per row), every row checked."""
+    """256 rows x 126464 bf16 -- the short-batch launch (16 waves per row), every row checked."""
     wl = WORKLOADS[2]
     d = decode_inputs(wl, seed_for(2))
     lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(2)).cuda()
@@ -114,6 +114,18 @@ def test_small_and_ragged_vocab(V):
     x = torch.from_numpy(rng.standard_normal((40, V)).astype(np.float32))
     for dt in (torch.float32, torch.bfloat16):
         _check(x.to(dt).cuda(), min(3, V), label=f"V={V} {dt}")
+
+
+# The two short-batch launches: 128..511 rows stream 32768 bf16 (16384 fp32) values per sweep,
+# 512..4095 rows 8192 (4096).  Each vocabulary gives 1, 3 or 5 whole sweeps (the two-sweep ring
+# with and without an odd remainder) plus a ragged tail of whole vectors and single values.
+@pytest.mark.parametrize("rows,V", [(130, 32776), (130, 98311), (130, 163848), (520, 8200), (520, 24583),
+                                    (520, 41000)])
+def test_short_batch_launches_ragged_vocab(rows, V):
+    rng = np.random.default_rng(rows * 7 + V)
+    x = torch.from_numpy(rng.standard_normal((rows, V)).astype(np.float32) * 2.0)
+    for dt in (torch.float32, torch.bfloat16):
+        _check(x.to(dt).cuda(), 3, label=f"rows={rows} V={V} {dt}")
 
 
 def test_negative_infinity_entries():
