@@ -232,11 +232,16 @@ __device__ __forceinline__ void mask_tail(f32x16_t& s, int key0, int S, int h) {
 template <int D>
 __device__ __forceinline__ f32x16_t qk_block(const uint16_t* kbase, const int (&kq)[D / 16],
                                              const bf16x8_t (&qf)[D / 16]) {
+    constexpr int KS = D / 16;
+    bf16x8_t ka[KS];
+    ka[0] = lds16(kbase + kq[0]);
+    ka[1] = lds16(kbase + kq[1]);
     f32x16_t s = {};
 #pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8_t a = lds16(kbase + kq[ks]);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s, 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks) {  // fragment reads two steps ahead, each after an MFMA
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], s, 0, 0, 0);
+        if (ks + 2 < KS) ka[ks + 2] = lds16(kbase + kq[ks + 2]);
+        __builtin_amdgcn_sched_barrier(0);
     }
     return s;
 }
@@ -246,14 +251,22 @@ __device__ __forceinline__ f32x16_t qk_block(const uint16_t* kbase, const int (&
 template <int D>
 __device__ __forceinline__ void pv_block(const uint16_t* vbase, const int (&vq)[D / 32], const bf16x8_t (&pf)[2],
                                          f32x16_t (&o)[D / 32]) {
+    constexpr int NDB = D / 32;
+    bf16x8_t va[2][NDB];
+    auto read_v = [&](int half, int db, bf16x8_t& dst) {
+        const bf16x4_t a0 = lds_read_tr(vbase + vq[db] + (16 * half) * D);
+        const bf16x4_t a1 = lds_read_tr(vbase + vq[db] + (16 * half + 8) * D);
+        dst = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int db = 0; db < NDB; ++db) read_v(0, db, va[0][db]);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-            const bf16x4_t a0 = lds_read_tr(vbase + vq[db] + (16 * half) * D);
-            const bf16x4_t a1 = lds_read_tr(vbase + vq[db] + (16 * half + 8) * D);
-            const bf16x8_t a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[half], o[db], 0, 0, 0);
+    for (int half = 0; half < 2; ++half) {  // the second half's reads follow the first half's MFMAs
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[half][db], pf[half], o[db], 0, 0, 0);
+            if (half == 0) read_v(1, db, va[1][db]);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 }
@@ -364,14 +377,16 @@ __device__ __forceinline__ void qk_pair(const uint16_t* kbase, const AttnLane<D>
         kb[ks] = lds16(kbase + 32 * D + ln.kq[ks]);
     }
     f32x16_t a = {}, b = {};
+    // Each fragment read is issued right after an MFMA, so that it issues while that MFMA
+    // executes: a wave issues in order and waits at an MFMA until the previous one has left the
+    // pipe, so reads placed after a run of MFMAs would add their issue time to the phase.
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-        if (ks + 2 < KS) {
-            ka[ks + 2] = lds16(kbase + ln.kq[ks + 2]);
-            kb[ks + 2] = lds16(kbase + 32 * D + ln.kq[ks + 2]);
-        }
         a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], a, 0, 0, 0);
+        if (ks + 2 < KS) ka[ks + 2] = lds16(kbase + ln.kq[ks + 2]);
+        __builtin_amdgcn_sched_barrier(0);
         b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[ks], qf[ks], b, 0, 0, 0);
+        if (ks + 2 < KS) kb[ks + 2] = lds16(kbase + 32 * D + ln.kq[ks + 2]);
         __builtin_amdgcn_sched_barrier(0);
     }
     sn[0] = a;
@@ -394,14 +409,79 @@ __device__ __forceinline__ void pv_pair(const uint16_t* vbase, const AttnLane<D>
             dst[db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
         }
     };
+    auto read_one = [&](int grp, int db, bf16x8_t& dst) {
+        const uint16_t* base = vbase + (grp >> 1) * 32 * D + (grp & 1) * 16 * D;
+        const bf16x4_t a0 = lds_read_tr(base + ln.vq[db]);
+        const bf16x4_t a1 = lds_read_tr(base + ln.vq[db] + 8 * D);
+        dst = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
     read_group(0, va[0]);
+    // the next group's reads go out one fragment after each MFMA (see qk_pair)
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp) {
-        if (grp + 1 < 4) read_group(grp + 1, va[(grp + 1) & 1]);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
+        for (int db = 0; db < NDB; ++db) {
             o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[grp & 1][db], pf[grp >> 1][grp & 1], o[db], 0, 0, 0);
+            if (grp + 1 < 4) read_one(grp + 1, db, va[(grp + 1) & 1][db]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// Matrix phase of a step with both parts: the scores of the next pair from the K rows at kbase
+// and O += V P of the current pair from the V rows at vbase.  As in qk_pair / pv_pair every
+// fragment read follows an MFMA; the V fragments of the first group ride on the last QK MFMAs,
+// which have no K reads left to carry.
+template <int D>
+__device__ __forceinline__ void matrix_pair(const uint16_t* kbase, const uint16_t* vbase, const AttnLane<D>& ln,
+                                            const bf16x8_t (&qf)[D / 16], f32x16_t (&sn)[2], const bf16x8_t (&pf)[2][2],
+                                            f32x16_t (&o)[D / 32]) {
+    constexpr int KS = D / 16;
+    constexpr int NDB = D / 32;
+    static_assert(2 * 2 >= NDB, "the last two QK steps carry the first V group");
+    bf16x8_t ka[KS], kb[KS];
+    bf16x8_t va[2][NDB];
+    auto read_v = [&](int grp, int db, bf16x8_t& dst) {
+        const uint16_t* base = vbase + (grp >> 1) * 32 * D + (grp & 1) * 16 * D;
+        const bf16x4_t a0 = lds_read_tr(base + ln.vq[db]);
+        const bf16x4_t a1 = lds_read_tr(base + ln.vq[db] + 8 * D);
+        dst = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        ka[ks] = lds16(kbase + ln.kq[ks]);
+        kb[ks] = lds16(kbase + 32 * D + ln.kq[ks]);
+    }
+    f32x16_t a = {}, b = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], a, 0, 0, 0);
+        if (ks + 2 < KS) {
+            ka[ks + 2] = lds16(kbase + ln.kq[ks + 2]);
+        } else {
+            const int db = 2 * (ks + 2 - KS);
+            if (db < NDB) read_v(0, db, va[0][db]);
+        }
         __builtin_amdgcn_sched_barrier(0);
+        b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[ks], qf[ks], b, 0, 0, 0);
+        if (ks + 2 < KS) {
+            kb[ks + 2] = lds16(kbase + 32 * D + ln.kq[ks + 2]);
+        } else {
+            const int db = 2 * (ks + 2 - KS) + 1;
+            if (db < NDB) read_v(0, db, va[0][db]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    sn[0] = a;
+    sn[1] = b;
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[grp & 1][db], pf[grp >> 1][grp & 1], o[db], 0, 0, 0);
+            if (grp + 1 < 4) read_v(grp + 1, db, va[(grp + 1) & 1][db]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 }
 
@@ -430,8 +510,7 @@ __device__ __forceinline__ void full_step(int t, const CacheArgs& a, const AttnL
     // the matrix phase issues at a raised wave priority: when the other wave on the SIMD is in
     // its softmax phase, the arbiter then keeps the matrix core fed first (-6% on 8b-batched)
     __builtin_amdgcn_s_setprio(1);
-    qk_pair<D>(cur, ln, qf, s);
-    pv_pair<D>(cur + G::kTileElems, ln, pf, o);
+    matrix_pair<D>(cur, cur + G::kTileElems, ln, qf, s, pf, o);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
@@ -609,13 +688,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
         softmax_phase<D>(s, c, thr, st, o, pf);
         __builtin_amdgcn_sched_barrier(0);
         if (2 * t + 2 < nb) {
-            qk_pair<D>(cur, ln, qf, s);
+            matrix_pair<D>(cur, cur + G::kTileElems, ln, qf, s, pf, o);
             if (64 * t + 128 > S) {
                 mask_tail(s[0], 64 * t + 64, S, h);
                 mask_tail(s[1], 64 * t + 96, S, h);
             }
+        } else {
+            pv_pair<D>(cur + G::kTileElems, ln, pf, o);
         }
-        pv_pair<D>(cur + G::kTileElems, ln, pf, o);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
     }
