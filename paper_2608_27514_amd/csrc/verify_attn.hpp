@@ -688,14 +688,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
         softmax_phase<D>(s, c, thr, st, o, pf);
         __builtin_amdgcn_sched_barrier(0);
         if (2 * t + 2 < nb) {
-            matrix_pair<D>(cur, cur + G::kTileElems, ln, qf, s, pf, o);
+            qk_pair<D>(cur, ln, qf, s);
             if (64 * t + 128 > S) {
                 mask_tail(s[0], 64 * t + 64, S, h);
                 mask_tail(s[1], 64 * t + 96, S, h);
             }
-        } else {
-            pv_pair<D>(cur + G::kTileElems, ln, pf, o);
         }
+        pv_pair<D>(cur + G::kTileElems, ln, pf, o);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
     }
