@@ -368,8 +368,9 @@ FLOOR_LIB = os.path.join(ROOT, "paper_2608_27514_amd", "libtrajfloor.so")
 def logit_floor(copies, stream, reps):
     """The logit pass's streaming-read floor on the same logit rows: libtrajfloor's read-only kernel
     with the launch shape the pass plans for this shape (workgroup size, load ring, row slices),
-    `reps` back-to-back launches over the rotated copies between two HIP events.  None when the
-    library is not built or the rows are not on the pass's 16-byte vector path."""
+    `reps` back-to-back launches over the rotated copies replayed as one HIP graph (graph_time),
+    like the pass in the configuration records.  None when the library is not built or the rows
+    are not on the pass's 16-byte vector path."""
     import ctypes
     if not os.path.exists(FLOOR_LIB):
         return None
@@ -382,57 +383,61 @@ def logit_floor(copies, stream, reps):
     wl = copies[0].wl
     sink = torch.zeros(4096, dtype=torch.int32, device=lg0.device)
     shape = (ctypes.c_int32 * 4)()
-    sp = ctypes.c_void_p(stream.cuda_stream)
 
-    def call(x):
+    def call(x, s):
         lg = x.logits
         return fn(ctypes.c_void_p(lg.data_ptr()), lg.shape[0], lg.shape[1], lg.stride(0), lg.element_size(),
-                  ctypes.c_void_p(sink.data_ptr()), shape, sp)
+                  ctypes.c_void_p(sink.data_ptr()), shape, ctypes.c_void_p(s.cuda_stream))
 
     n = len(copies)
-    if call(copies[0]) != 0:
+    if call(copies[0], stream) != 0:
         return None
-    for i in range(3):
-        call(copies[i % n])
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for i in range(reps):
-        call(copies[i % n])
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    ms = graph_time(lambda i, s: call(copies[i % n], s), stream, reps)
     gbs = logit_bytes(wl) / (ms * 1e-3) / 1e9
     return {"kernel": "read-only floor (libtrajfloor), same launch shape and loads as the pass",
             "launch": {"threads": shape[0], "unroll": shape[1], "depth": shape[2], "row_slices": shape[3]},
             "us": ms * 1e3, "gbs": gbs, "frac_of_hbm": gbs / PEAK_HBM_GBS}
 
 
+def graph_time(launch, stream, reps):
+    """Per-launch ms of `reps` back-to-back launches (launch(i, s) enqueues the i-th on torch
+    stream s), captured once in a HIP graph on a side stream and replayed between two HIP events
+    on `stream`: the time the kernel takes in a steady stream of launches, without the host issue
+    of each call or the dispatch gap between separately issued launches (both matter for kernels
+    of tens of microseconds).  The library's entry points only enqueue kernels, so they are
+    capturable."""
+    for i in range(3):
+        launch(i, stream)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        for i in range(reps):
+            launch(i, side)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) / reps
+
+
 def time_kernels_apart(copies, buf, tau, stream, reps):
-    """Each kernel of the step on its own: `reps` back-to-back launches over the rotated copies
-    between two HIP events (the per-call event pairs of the step timing add their own overhead,
-    which matters for kernels of tens of microseconds).  Returns per-launch ms."""
+    """Each kernel of the step on its own: `reps` back-to-back launches over the rotated copies,
+    timed as one replayed HIP graph (graph_time).  Returns per-launch ms."""
     n = len(copies)
     calls = {
-        "verify_attn": lambda x: tsp.verify_attn(x.q, x.kc, x.vc, x.kd, x.vd, x.parent, out=buf.out, stream=stream),
-        "confidence_topk": lambda x: tsp.confidence_topk(x.logits, x.wl.k, conf=buf.conf, idx=buf.idx,
-                                                         workspace=buf.ws, stream=stream),
-        "accept": lambda x: tsp.accept(buf.conf, buf.idx, x.tokens, x.parent, x.committed, x.conf0, x.idx0, tau,
-                                       out=buf.acc, stream=stream),
+        "verify_attn": lambda x, s: tsp.verify_attn(x.q, x.kc, x.vc, x.kd, x.vd, x.parent, out=buf.out, stream=s),
+        "confidence_topk": lambda x, s: tsp.confidence_topk(x.logits, x.wl.k, conf=buf.conf, idx=buf.idx,
+                                                            workspace=buf.ws, stream=s),
+        "accept": lambda x, s: tsp.accept(buf.conf, buf.idx, x.tokens, x.parent, x.committed, x.conf0, x.idx0, tau,
+                                          out=buf.acc, stream=s),
     }
-    out = {}
-    for name, fn in calls.items():
-        for i in range(3):
-            fn(copies[i % n])
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for i in range(reps):
-            fn(copies[i % n])
-        e1.record(stream)
-        torch.cuda.synchronize()
-        out[name] = e0.elapsed_time(e1) / reps
-    return out
+    return {name: graph_time(lambda i, s, fn=fn: fn(copies[i % n], s), stream, reps) for name, fn in calls.items()}
 
 
 def time_config(cid, stream, steps, warmup):

@@ -136,13 +136,15 @@ __device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
     return best;
 }
 
-// The K best keys of a wave (descending, in every lane) from the lanes' sorted lists, by K
-// rounds of a wave-wide maximum over the list heads; the lane holding the winner drops it
-// (keys are unique: the index is part of the key).
+// The k <= K best keys of a wave (descending, in every lane; the others 0) from the lanes' sorted
+// lists, by k rounds of a wave-wide maximum over the list heads; the lane holding the winner
+// drops it (keys are unique: the index is part of the key).
 template <int K>
-__device__ __forceinline__ void wave_top_keys(TopList<K>& tl, uint64_t (&best)[K]) {
+__device__ __forceinline__ void wave_top_keys(TopList<K>& tl, uint64_t (&best)[K], int k) {
 #pragma unroll
     for (int r = 0; r < K; ++r) {
+        best[r] = 0ull;
+        if (r >= k) continue;  // wave-uniform
         const uint64_t head = tl.key[0];
         uint64_t mk = head;
 #pragma unroll
@@ -288,7 +290,9 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) absorb<K, NV>(x[u], vm[u], begin + (sweep * SW + u * THREADS + tid) * NV, st, floor_bits);
-            if ((sweep & (sweep + 1)) == 0) {  // after sweeps 0, 1, 3, 7, ...
+            // after sweeps 1, 3, 7, ... (after sweep 0 the lane maxima are those the first floor
+            // was taken from)
+            if (sweep != 0 && (sweep & (sweep + 1)) == 0) {
                 floor_bits = wave_kth_floor<K>(st.lmax, k);
                 st.refresh(floor_bits);
             }
@@ -341,7 +345,7 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
     uint64_t best[K];
-    wave_top_keys<K>(st.tl, best);
+    wave_top_keys<K>(st.tl, best, k);
     // waves -> workgroup
     constexpr int NW = THREADS / 64;
     TopList<K> tl;
@@ -422,7 +426,7 @@ __global__ __launch_bounds__(64) void conf_topk_merge_kernel(const float* __rest
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
     uint64_t best[K];
-    wave_top_keys<K>(tl, best);
+    wave_top_keys<K>(tl, best, k);
     if (lane != 0) return;
     const float inv = 1.0f / s;
 #pragma unroll
