@@ -20,9 +20,10 @@
 //     when its maximum reaches max(wave floor, the lane's k-th key), kept as one float.  The wave
 //     floor is a lower bound on the row's k-th largest value (the k-th largest lane maximum),
 //     first taken from sweep 0 before anything is absorbed, then after sweeps 1, 3, 7, ...;
-//   * lanes merge (reference, sum) by shuffles and their keys by k rounds of a wave-wide
-//     maximum, waves through LDS; row slices write (reference, sum, top-K) partial records that
-//     a second one-wave-per-row kernel merges with the same associative rule.
+//   * lanes merge (reference, sum) and take the wave's keys by k rounds of a wave-wide maximum,
+//     both over the DPP / permlane exchange network (no LDS round trips), waves through LDS; row
+//     slices write (reference, sum, top-K) partial records that a second one-wave-per-row kernel
+//     merges with the same associative rule.
 #pragma once
 
 #include "common.hpp"
@@ -97,10 +98,60 @@ struct TopList {
     }
 };
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int off) {
-    const uint32_t lo = __shfl_xor((uint32_t)x, off);
-    const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), off);
-    return ((uint64_t)hi << 32) | lo;
+// Wave reductions run on the lane-exchange network rather than through the LDS crossbar
+// (ds_bpermute).  At step t every lane receives two values a, b to combine, its own and a
+// partner's in some order: t = 0, 1 pair lanes 1 and 2 apart inside quads (DPP quad
+// permutations); t = 2, 3 take the lane 4 and 8 below in the row of 16, cyclically (DPP row
+// rotations: once the lanes of each quad agree they combine whole quads); t = 4 pairs rows 0 with
+// 1 and 2 with 3, t = 5 the two halves of the wave (gfx950 permlane swaps, which hand each lane
+// both values).  Combining with a commutative, associative operation at steps 0 .. 5 leaves the
+// wave's result in every lane; steps 0 .. 3 alone reduce each row of 16 lanes.
+__device__ __forceinline__ void lane_pair(int step, uint32_t v, uint32_t& a, uint32_t& b) {
+    const int iv = (int)v;
+    switch (step) {  // a compile-time constant wherever this is inlined into an unrolled loop
+    case 0: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0xB1, 0xF, 0xF, false); break;  // quad [1,0,3,2]
+    case 1: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x4E, 0xF, 0xF, false); break;  // quad [2,3,0,1]
+    case 2: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x124, 0xF, 0xF, false); break;  // row_ror:4
+    case 3: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x128, 0xF, 0xF, false); break;  // row_ror:8
+    case 4: {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        a = r[0];
+        b = r[1];
+        break;
+    }
+    default: {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        a = r[0];
+        b = r[1];
+        break;
+    }
+    }
+}
+__device__ __forceinline__ void lane_pair64(int step, uint64_t v, uint64_t& a, uint64_t& b) {
+    uint32_t ah, bh, al, bl;
+    lane_pair(step, (uint32_t)(v >> 32), ah, bh);
+    lane_pair(step, (uint32_t)v, al, bl);
+    a = ((uint64_t)ah << 32) | al;
+    b = ((uint64_t)bh << 32) | bl;
+}
+// Unsigned maxima over the wave, in every lane.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+        uint32_t a, b;
+        lane_pair(t, v, a, b);
+        v = a > b ? a : b;
+    }
+    return v;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+        uint64_t a, b;
+        lane_pair64(t, v, a, b);
+        v = kmax(a, b);
+    }
+    return v;
 }
 
 // Merge two (reference, sum) pairs, each sum relative to its own reference; the result is
@@ -110,6 +161,21 @@ __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2)
     const float Ms = fmaxf(M, -1e30f);
     s = s * fast_exp2((m - Ms) * kLog2e) + s2 * fast_exp2((m2 - Ms) * kLog2e);
     m = M;
+}
+
+// (reference, sum) pairs combined over exchange steps 0 .. STEPS-1 (6: the wave, 4: each row of
+// 16 lanes).  Lanes may round differently (the combination order differs); lane 0 holds a result.
+template <int STEPS>
+__device__ __forceinline__ void lanes_merge_ms(float& m, float& s) {
+#pragma unroll
+    for (int t = 0; t < STEPS; ++t) {
+        uint32_t am, bm, as, bs;
+        lane_pair(t, __builtin_bit_cast(uint32_t, m), am, bm);
+        lane_pair(t, __builtin_bit_cast(uint32_t, s), as, bs);
+        m = __builtin_bit_cast(float, am);
+        s = __builtin_bit_cast(float, as);
+        merge_ms(m, s, __builtin_bit_cast(float, bm), __builtin_bit_cast(float, bs));
+    }
 }
 
 // Lower bound on the k-th largest value of a row from the lanes' maxima: the k-th largest lane
@@ -124,12 +190,7 @@ __device__ __forceinline__ uint32_t wave_kth_floor(float lane_max, int k) {
 #pragma unroll
     for (int r = 0; r < K; ++r) {
         if (r < k) {
-            best = cur;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                const uint32_t o = __shfl_xor(best, off);
-                best = o > best ? o : best;
-            }
+            best = wave_max_u32(cur);
             if (cur == best) cur = 0u;
         }
     }
@@ -146,9 +207,7 @@ __device__ __forceinline__ void wave_top_keys(TopList<K>& tl, uint64_t (&best)[K
         best[r] = 0ull;
         if (r >= k) continue;  // wave-uniform
         const uint64_t head = tl.key[0];
-        uint64_t mk = head;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) mk = kmax(mk, shfl_xor64(mk, off));
+        const uint64_t mk = wave_max_u64(head);
         best[r] = mk;
         if (r + 1 < K && head == mk && mk != 0ull) {
 #pragma unroll
@@ -271,6 +330,28 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
     st.init();
     uint32_t floor_bits = 0;
     int scalar_from = begin;
+    // The waves of a workgroup share their floors through LDS: each floor is a lower bound on the
+    // row's k-th largest value, so the largest of them is one too and gates every wave's
+    // insertions.  A value read before another wave updates its word is merely a weaker bound,
+    // so no barrier orders the accesses (only the initial zeros).
+    constexpr int NWR = THREADS / 64;
+    __shared__ uint32_t sh_floor[NWR];
+    if (NWR > 1) {
+        if ((tid & 63) == 0) sh_floor[tid >> 6] = 0u;
+        __syncthreads();
+    }
+    auto share_floor = [&](uint32_t fb) {  // publish fb, return the largest floor of the workgroup
+        if (NWR > 1) {
+            if ((tid & 63) == 0)
+                __hip_atomic_store(&sh_floor[tid >> 6], fb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+            for (int w = 0; w < NWR; ++w) {
+                const uint32_t o = __hip_atomic_load(&sh_floor[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                fb = o > fb ? o : fb;
+            }
+        }
+        return fb;
+    };
     if (VECTOR) {
         const int nvec = (end - begin) / NV;
         const int nfull = nvec / SW;
@@ -293,8 +374,15 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
             // after sweeps 1, 3, 7, ... (after sweep 0 the lane maxima are those the first floor
             // was taken from)
             if (sweep != 0 && (sweep & (sweep + 1)) == 0) {
-                floor_bits = wave_kth_floor<K>(st.lmax, k);
+                const uint32_t own = wave_kth_floor<K>(st.lmax, k);
+                floor_bits = share_floor(own > floor_bits ? own : floor_bits);
                 st.refresh(floor_bits);
+            } else if (NWR > 1) {  // pick up the other waves' floors every sweep
+                const uint32_t f = share_floor(floor_bits);
+                if (f != floor_bits) {  // wave-uniform
+                    floor_bits = f;
+                    st.refresh(floor_bits);
+                }
             }
         };
         if (nfull > 0) {
@@ -309,7 +397,7 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
                     unpack(buf[0][u], x0);
                     lm = __builtin_elementwise_maximum(lm, vec_max<NV>(x0));
                 }
-                floor_bits = wave_kth_floor<K>(lm, k);
+                floor_bits = share_floor(wave_kth_floor<K>(lm, k));
                 st.refresh(floor_bits);
             }
             int it = 0;
@@ -340,10 +428,10 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
         absorb<K, 1>(x, x[0], e, st, floor_bits);
     }
 
-    // lanes -> wave: (reference, sum) by shuffles, the keys by K rounds of a wave maximum
+    // lanes -> wave: (reference, sum) over the exchange network, the keys by k rounds of a wave
+    // maximum
     float m = st.ref, s = st.s;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
+    lanes_merge_ms<6>(m, s);
     uint64_t best[K];
     wave_top_keys<K>(st.tl, best, k);
     // waves -> workgroup
@@ -374,13 +462,17 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
             s = 0.f;
             tl.clear();
         }
+        // lanes 0 .. NW-1 hold the waves' results, lanes NW .. 15 neutral ones: a reduction over
+        // the quad steps (NW <= 4) or the row of 16 leaves the workgroup's in lane 0
+        constexpr int STEPS = NW <= 2 ? 1 : NW <= 4 ? 2 : 4;
+        static_assert(NW <= 16, "the row reduction covers at most 16 waves");
+        lanes_merge_ms<STEPS>(m, s);
 #pragma unroll
-        for (int off = NW / 2; off >= 1; off >>= 1) {
-            merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
-            uint64_t o[K];
+        for (int t = 0; t < STEPS; ++t) {
+            uint64_t b[K];
 #pragma unroll
-            for (int j = 0; j < K; ++j) o[j] = shfl_xor64(tl.key[j], off);
-            tl.merge(o);
+            for (int j = 0; j < K; ++j) lane_pair64(t, tl.key[j], tl.key[j], b[j]);
+            tl.merge(b);
         }
     }
     if (lane != 0) return;
@@ -423,8 +515,7 @@ __global__ __launch_bounds__(64) void conf_topk_merge_kernel(const float* __rest
         for (int j = 0; j < K; ++j) o[j] = rk[j];
         tl.merge(o);
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) merge_ms(m, s, __shfl_xor(m, off), __shfl_xor(s, off));
+    lanes_merge_ms<6>(m, s);
     uint64_t best[K];
     wave_top_keys<K>(tl, best, k);
     if (lane != 0) return;
