@@ -20,6 +20,7 @@ import argparse
 import json
 import math
 import os
+import statistics
 import sys
 import time
 
@@ -399,13 +400,15 @@ def logit_floor(copies, stream, reps):
             "us": ms * 1e3, "gbs": gbs, "frac_of_hbm": gbs / PEAK_HBM_GBS}
 
 
-def graph_time(launch, stream, reps):
+def graph_time(launch, stream, reps, replays=5):
     """Per-launch ms of `reps` back-to-back launches (launch(i, s) enqueues the i-th on torch
     stream s), captured once in a HIP graph on a side stream and replayed between two HIP events
     on `stream`: the time the kernel takes in a steady stream of launches, without the host issue
     of each call or the dispatch gap between separately issued launches (both matter for kernels
-    of tens of microseconds).  The library's entry points only enqueue kernels, so they are
-    capturable."""
+    of tens of microseconds).  One replay of a few milliseconds varies by several percent from
+    one replay to the next (clock and memory state), so the median over `replays` timed replays
+    (after one untimed) is reported.  The library's entry points only enqueue kernels, so they
+    are capturable."""
     for i in range(3):
         launch(i, stream)
     torch.cuda.synchronize()
@@ -417,13 +420,16 @@ def graph_time(launch, stream, reps):
     torch.cuda.synchronize()
     g.replay()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    g.replay()
-    e1.record(stream)
-    torch.cuda.synchronize()
+    times = []
+    for _ in range(replays):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / reps)
     del g
-    return e0.elapsed_time(e1) / reps
+    return statistics.median(times)
 
 
 def time_kernels_apart(copies, buf, tau, stream, reps):
