@@ -1,15 +1,18 @@
 // Acceptance of the longest consistent trajectory (Sec. 3.3 "Verification procedure"),
 // with the threshold-decoding step of Sec. 2.1 and the high-confidence set of Alg. 1
-// phase 1.  One 256-thread workgroup per sequence; every per-state / per-draft test is a
-// 64-lane wave operation (lane = block position, L <= 64), the walk is a loop of wave
-// ballots (lane = draft, N <= 64).
+// phase 1.  One 1024-thread workgroup per sequence.  The kernel is latency-bound: every input
+// it reads (draft tokens, their top-1 confidences and tokens, the committed state, the parents)
+// is first staged into LDS in one round of independent loads, so the sequence pays one memory
+// latency instead of one per state and per draft; every per-state / per-draft test is then a
+// 64-lane wave operation on LDS (lane = block position, L <= 64, 16 waves in parallel), and the
+// walk is a loop of wave ballots (lane = draft, N <= 64).
 #pragma once
 
 #include "common.hpp"
 
 namespace trajspec {
 
-constexpr int kAcceptThreads = 256;
+constexpr int kAcceptThreads = 1024;
 constexpr int kMaxDrafts = 64;
 constexpr int kMaxBlock = 64;
 
@@ -30,7 +33,30 @@ struct AcceptParams {
     float tau;
 };
 
+// The wave's best (value, position) pair in every lane: the larger value, then the smaller
+// position (T = float or int; positions are non-negative).
+template <typename T>
+__device__ __forceinline__ void wave_argmax(T& v, int& pos) {
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+        uint32_t av, bv, ap, bp;
+        lane_pair(t, __builtin_bit_cast(uint32_t, v), av, bv);
+        lane_pair(t, (uint32_t)pos, ap, bp);
+        const T va = __builtin_bit_cast(T, av), vb = __builtin_bit_cast(T, bv);
+        const bool take_b = vb > va || (vb == va && (int)bp < (int)ap);
+        v = take_b ? vb : va;
+        pos = take_b ? (int)bp : (int)ap;
+    }
+}
+
 __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) {
+    // staged inputs, [n * L + p] for draft n (the committed state separately)
+    __shared__ int tok[kMaxDrafts * kMaxBlock];
+    __shared__ float top_c[kMaxDrafts * kMaxBlock];
+    __shared__ int top_t[kMaxDrafts * kMaxBlock];
+    __shared__ int s0[kMaxBlock];
+    __shared__ float c0[kMaxBlock];
+    __shared__ int t0[kMaxBlock];
     __shared__ int par[kMaxDrafts];
     __shared__ int expected[kMaxDrafts + 1][kMaxBlock];
     __shared__ int has_step[kMaxDrafts + 1];
@@ -43,17 +69,58 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
     const int wave = tid >> 6;
     constexpr int NW = kAcceptThreads / 64;
     const int N = P.N, L = P.L, k = P.k;
+    const int NL = N * L;
     const int32_t MASK = -1;
 
-    // Parents: anything outside [-1, n) is reported and treated as -1.
-    for (int n = tid; n < N; n += kAcceptThreads) {
-        int q = P.parent[(int64_t)b * N + n];
-        if (q < -1 || q >= n) {
-            flag_device_status(1);
-            q = -1;
+    // Stage: at most kMaxDrafts * kMaxBlock / kAcceptThreads = 4 elements of each draft array
+    // per thread, all loads issued before any is used.
+    {
+        constexpr int R = kMaxDrafts * kMaxBlock / kAcceptThreads;
+        const int64_t base = (int64_t)b * NL;
+        int vt[R], vi[R];
+        float vc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int e = tid + r * kAcceptThreads;
+            if (e < NL) {
+                vt[r] = P.tokens[base + e];
+                vc[r] = P.conf[(base + e) * k];
+                vi[r] = P.idx[(base + e) * k];
+            }
         }
-        par[n] = q;
+        int q = -1, cs = 0, ct = 0;
+        float cc = 0.f;
+        if (tid < N) q = P.parent[(int64_t)b * N + tid];
+        if (tid < L) {
+            const int64_t o = (int64_t)b * L + tid;
+            cs = P.committed[o];
+            cc = P.conf0[o * k];
+            ct = P.idx0[o * k];
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int e = tid + r * kAcceptThreads;
+            if (e < NL) {
+                tok[e] = vt[r];
+                top_c[e] = vc[r];
+                top_t[e] = vi[r];
+            }
+        }
+        // Parents: anything outside [-1, n) is reported and treated as -1.
+        if (tid < N) {
+            if (q < -1 || q >= tid) {
+                flag_device_status(1);
+                q = -1;
+            }
+            par[tid] = q;
+        }
+        if (tid < L) {
+            s0[tid] = cs;
+            c0[tid] = cc;
+            t0[tid] = ct;
+        }
     }
+    __syncthreads();
 
     // Threshold step of every state q in [-1, N): one wave per state, one lane per position.
     const bool lane_in = lane < L;
@@ -62,15 +129,13 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
         float c = 0.f;
         if (lane_in) {
             if (q < 0) {
-                const int64_t o = (int64_t)b * L + lane;
-                s = P.committed[o];
-                c = P.conf0[o * k];
-                t1 = P.idx0[o * k];
+                s = s0[lane];
+                c = c0[lane];
+                t1 = t0[lane];
             } else {
-                const int64_t o = ((int64_t)b * N + q) * L + lane;
-                s = P.tokens[o];
-                c = P.conf[o * k];
-                t1 = P.idx[o * k];
+                s = tok[q * L + lane];
+                c = top_c[q * L + lane];
+                t1 = top_t[q * L + lane];
             }
         }
         const bool masked = lane_in && s == MASK;
@@ -83,15 +148,7 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
             // fallback: most confident masked position, smallest position on ties
             float bc = masked ? c : -1.0f;
             int bp = masked ? lane : 0x7fffffff;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                const float oc = __shfl_xor(bc, off);
-                const int op = __shfl_xor(bp, off);
-                if (oc > bc || (oc == bc && op < bp)) {
-                    bc = oc;
-                    bp = op;
-                }
-            }
+            wave_argmax(bc, bp);
             chosen = lane == bp;
         }
         if (lane_in) expected[q + 1][lane] = chosen ? t1 : s;
@@ -102,11 +159,11 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
     // Consistency of every draft with its parent state; gain w.r.t. the committed state.
     for (int cnode = wave; cnode < N; cnode += NW) {
         const int q = par[cnode];
-        int t = MASK, sp = MASK, s0 = MASK;
+        int t = MASK, sp = MASK, sc = MASK;
         if (lane_in) {
-            t = P.tokens[((int64_t)b * N + cnode) * L + lane];
-            s0 = P.committed[(int64_t)b * L + lane];
-            sp = q < 0 ? s0 : P.tokens[((int64_t)b * N + q) * L + lane];
+            t = tok[cnode * L + lane];
+            sc = s0[lane];
+            sp = q < 0 ? sc : tok[q * L + lane];
         }
         bool ok;
         bool ok_all;
@@ -131,7 +188,7 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
             }
             ok_all = ballot64(!ok) == 0 && ballot64(isnew) != 0;
         }
-        const uint64_t gm = ballot64(lane_in && s0 == MASK && t != MASK);
+        const uint64_t gm = ballot64(lane_in && sc == MASK && t != MASK);
         if (lane == 0) {
             consistent[cnode] = ok_all ? 1 : 0;
             gain[cnode] = __popcll(gm);
@@ -164,23 +221,14 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(AcceptParams P) 
         const bool v = node_in && ((valid >> lane) & 1ull);
         int bg = v ? gain[lane] : -1;
         int bn = v ? lane : 0x7fffffff;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const int og = __shfl_xor(bg, off);
-            const int on = __shfl_xor(bn, off);
-            if (og > bg || (og == bg && on < bn)) {
-                bg = og;
-                bn = on;
-            }
-        }
+        wave_argmax(bg, bn);
         leaf = bg >= 0 ? bn : -1;
     }
     uint64_t path = 0;
     for (int j = leaf, hops = 0; j >= 0 && hops <= N; j = par[j], ++hops) path |= 1ull << j;
     if (node_in) P.on_path[(int64_t)b * N + lane] = (path >> lane) & 1ull ? 1 : 0;
     if (lane_in) {
-        P.out_tokens[(int64_t)b * L + lane] =
-            leaf >= 0 ? P.tokens[((int64_t)b * N + leaf) * L + lane] : P.committed[(int64_t)b * L + lane];
+        P.out_tokens[(int64_t)b * L + lane] = leaf >= 0 ? tok[leaf * L + lane] : s0[lane];
     }
     if (lane == 0) {
         P.leaf[b] = leaf;

@@ -98,35 +98,6 @@ struct TopList {
     }
 };
 
-// Wave reductions run on the lane-exchange network rather than through the LDS crossbar
-// (ds_bpermute).  At step t every lane receives two values a, b to combine, its own and a
-// partner's in some order: t = 0, 1 pair lanes 1 and 2 apart inside quads (DPP quad
-// permutations); t = 2, 3 take the lane 4 and 8 below in the row of 16, cyclically (DPP row
-// rotations: once the lanes of each quad agree they combine whole quads); t = 4 pairs rows 0 with
-// 1 and 2 with 3, t = 5 the two halves of the wave (gfx950 permlane swaps, which hand each lane
-// both values).  Combining with a commutative, associative operation at steps 0 .. 5 leaves the
-// wave's result in every lane; steps 0 .. 3 alone reduce each row of 16 lanes.
-__device__ __forceinline__ void lane_pair(int step, uint32_t v, uint32_t& a, uint32_t& b) {
-    const int iv = (int)v;
-    switch (step) {  // a compile-time constant wherever this is inlined into an unrolled loop
-    case 0: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0xB1, 0xF, 0xF, false); break;  // quad [1,0,3,2]
-    case 1: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x4E, 0xF, 0xF, false); break;  // quad [2,3,0,1]
-    case 2: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x124, 0xF, 0xF, false); break;  // row_ror:4
-    case 3: a = v; b = (uint32_t)__builtin_amdgcn_update_dpp(iv, iv, 0x128, 0xF, 0xF, false); break;  // row_ror:8
-    case 4: {
-        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        a = r[0];
-        b = r[1];
-        break;
-    }
-    default: {
-        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-        a = r[0];
-        b = r[1];
-        break;
-    }
-    }
-}
 __device__ __forceinline__ void lane_pair64(int step, uint64_t v, uint64_t& a, uint64_t& b) {
     uint32_t ah, bh, al, bl;
     lane_pair(step, (uint32_t)(v >> 32), ah, bh);
