@@ -5,9 +5,10 @@
 // HBM-bound streaming design for gfx950:
 //   * one workgroup streams one row (or one slice of a row when there are very few rows) with
 //     16-byte non-temporal loads held in a register ring: DEPTH sweeps of U vectors per lane,
-//     DEPTH - 1 of them in flight while one is absorbed.  The main loop runs whole groups of
-//     DEPTH sweeps with unconditional loads (past the end a lane reloads the last sweep and
-//     discards it), so the compiler's load waits count exactly the older loads;
+//     DEPTH - 1 of them in flight while one is absorbed.  The loop runs whole groups of DEPTH
+//     sweeps with unconditional loads (vector indices past the row are clamped to its last
+//     vector and discarded), so the compiler's load waits count exactly the older loads; the
+//     row's last, partial sweep goes through the same ring, in flight behind the last full one;
 //   * the workgroup size follows the row count: one wave per row for large batches (many
 //     resident workgroups per CU), 4 to 16 waves per row for short batches so that the launch
 //     still holds about four waves per SIMD;
@@ -25,6 +26,8 @@
 //     slices write (reference, sum, top-K) partial records that a second one-wave-per-row kernel
 //     merges with the same associative rule.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -326,13 +329,22 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
     if (VECTOR) {
         const int nvec = (end - begin) / NV;
         const int nfull = nvec / SW;
+        const bool tail = nvec > nfull * SW;  // a last, partial sweep (fewer than SW vectors)
+        const int nsw = nfull + (tail ? 1 : 0);
         const u32x4_t* vp = reinterpret_cast<const u32x4_t*>(base + begin);
+        // Vector indices past the row are clamped to its last vector: such loads (the partial
+        // sweep's missing vectors, the ring's loads beyond the last sweep) hit one cache line
+        // and are never absorbed.
         auto load = [&](int sweep, u32x4_t (&b)[U]) {
-            const int sw = sweep < nfull ? sweep : nfull - 1;  // past the end: the last sweep again
 #pragma unroll
-            for (int u = 0; u < U; ++u) b[u] = __builtin_nontemporal_load(vp + sw * SW + u * THREADS + tid);
+            for (int u = 0; u < U; ++u) {
+                const int v = sweep * SW + u * THREADS + tid;
+                b[u] = __builtin_nontemporal_load(vp + (v < nvec ? v : nvec - 1));
+            }
         };
-        auto absorb_sweep = [&](int sweep, const u32x4_t (&b)[U]) {
+        // PARTIAL: only the row's last sweep, whose vectors past the row are skipped.
+        auto absorb_sweep = [&](int sweep, const u32x4_t (&b)[U], auto partial_tag) {
+            constexpr bool PARTIAL = decltype(partial_tag)::value;
             float x[U][NV];
             float vm[U];
 #pragma unroll
@@ -341,7 +353,10 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
                 vm[u] = vec_max<NV>(x[u]);
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) absorb<K, NV>(x[u], vm[u], begin + (sweep * SW + u * THREADS + tid) * NV, st, floor_bits);
+            for (int u = 0; u < U; ++u) {
+                const int v = sweep * SW + u * THREADS + tid;
+                if (!PARTIAL || v < nvec) absorb<K, NV>(x[u], vm[u], begin + v * NV, st, floor_bits);
+            }
             // after sweeps 1, 3, 7, ... (after sweep 0 the lane maxima are those the first floor
             // was taken from)
             if (sweep != 0 && (sweep & (sweep + 1)) == 0) {
@@ -356,7 +371,9 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
                 }
             }
         };
-        if (nfull > 0) {
+        using Full = std::integral_constant<bool, false>;
+        using Partial = std::integral_constant<bool, true>;
+        if (nsw > 0) {
             u32x4_t buf[DEPTH][U];
 #pragma unroll
             for (int d = 0; d + 1 < DEPTH; ++d) load(d, buf[d]);
@@ -366,7 +383,8 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
                 for (int u = 0; u < U; ++u) {
                     float x0[NV];
                     unpack(buf[0][u], x0);
-                    lm = __builtin_elementwise_maximum(lm, vec_max<NV>(x0));
+                    const bool in_row = u * THREADS + tid < nvec;  // false only in a partial sweep 0
+                    lm = __builtin_elementwise_maximum(lm, in_row ? vec_max<NV>(x0) : kNegInf);
                 }
                 floor_bits = share_floor(wave_kth_floor<K>(lm, k));
                 st.refresh(floor_bits);
@@ -377,20 +395,24 @@ __global__ __launch_bounds__(THREADS) void conf_topk_kernel(const T* __restrict_
                 for (int j = 0; j < DEPTH; ++j) {
                     load(it + j + DEPTH - 1, buf[(j + DEPTH - 1) % DEPTH]);
                     __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the absorb
-                    absorb_sweep(it + j, buf[j]);
+                    absorb_sweep(it + j, buf[j], Full{});
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            // the remaining nfull - it < DEPTH sweeps are already in buf[0 ..]
+            // The remaining nfull - it < DEPTH full sweeps and the partial one: one more group of
+            // the same shape (its loads unconditional, so the load waits stay exact), the partial
+            // sweep in flight behind the last full one.
 #pragma unroll
-            for (int j = 0; j + 1 < DEPTH; ++j)
-                if (it + j < nfull) absorb_sweep(it + j, buf[j]);
-        }
-        // last, partial sweep: one vector at a time
-        for (int v = nfull * SW + tid; v < nvec; v += THREADS) {
-            float x[NV];
-            unpack(__builtin_nontemporal_load(vp + v), x);
-            absorb<K, NV>(x, vec_max<NV>(x), begin + v * NV, st, floor_bits);
+            for (int j = 0; j < DEPTH; ++j) {
+                load(it + j + DEPTH - 1, buf[(j + DEPTH - 1) % DEPTH]);
+                __builtin_amdgcn_sched_barrier(0);
+                if (it + j < nfull) {
+                    absorb_sweep(it + j, buf[j], Full{});
+                } else if (it + j < nsw) {
+                    absorb_sweep(it + j, buf[j], Partial{});
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         scalar_from = begin + nvec * NV;
     }

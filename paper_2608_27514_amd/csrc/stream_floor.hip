@@ -4,8 +4,9 @@
 // The kernel reads rows of bytes with exactly the launch shape and load pattern of the logit pass
 // (conf_topk.hpp): one workgroup per row, THREADS lanes, 16-byte non-temporal loads held in a ring
 // of DEPTH sweeps of U vectors per lane, unconditional loads in a loop over whole groups of DEPTH
-// sweeps.  Instead of the softmax and the top-k it only XORs the words it reads (so the loads stay
-// live) and writes one word per wave.  Its duration on the same rows is what the memory system
+// sweeps, the row's last partial sweep loaded through the same ring.  Instead of the softmax and
+// the top-k it only XORs the words it reads (so the loads stay live) and writes one word per
+// wave.  Its duration on the same rows is what the memory system
 // delivers to that access pattern: the logit pass's time against it separates the cost of the
 // arithmetic from the cost of the reads.
 #include <hip/hip_runtime.h>
@@ -31,14 +32,23 @@ __global__ __launch_bounds__(THREADS) void stream_floor_kernel(const u32x4* __re
     const u32x4* vp = data + (int64_t)row * row_stride_vec + begin;
     const int tid = threadIdx.x;
     const int nfull = nvec / SW;
+    const bool tail = nvec > nfull * SW;
+    const int nsw = nfull + (tail ? 1 : 0);
     uint32_t acc = 0;
     auto take = [&](const u32x4& w) { acc ^= w[0] ^ w[1] ^ w[2] ^ w[3]; };
-    if (nfull > 0) {
+    if (nsw > 0) {
         u32x4 buf[DEPTH][U];
-        auto load = [&](int sweep, u32x4 (&b)[U]) {
-            const int sw = sweep < nfull ? sweep : nfull - 1;
+        auto load = [&](int sweep, u32x4 (&b)[U]) {  // indices past the row clamped to its last vector
 #pragma unroll
-            for (int u = 0; u < U; ++u) b[u] = __builtin_nontemporal_load(vp + sw * SW + u * THREADS + tid);
+            for (int u = 0; u < U; ++u) {
+                const int v = sweep * SW + u * THREADS + tid;
+                b[u] = __builtin_nontemporal_load(vp + (v < nvec ? v : nvec - 1));
+            }
+        };
+        auto take_sweep = [&](int sweep, const u32x4 (&b)[U], bool partial) {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (!partial || sweep * SW + u * THREADS + tid < nvec) take(b[u]);
         };
 #pragma unroll
         for (int d = 0; d + 1 < DEPTH; ++d) load(d, buf[d]);
@@ -48,22 +58,25 @@ __global__ __launch_bounds__(THREADS) void stream_floor_kernel(const u32x4* __re
             for (int j = 0; j < DEPTH; ++j) {
                 load(it + j + DEPTH - 1, buf[(j + DEPTH - 1) % DEPTH]);
                 __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int u = 0; u < U; ++u) take(buf[j][u]);
+                take_sweep(it + j, buf[j], false);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+        // the remaining full sweeps and the partial one, as one more group with unconditional loads
 #pragma unroll
-        for (int j = 0; j + 1 < DEPTH; ++j) {
-            if (it + j < nfull) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) take(buf[j][u]);
-            }
+        for (int j = 0; j < DEPTH; ++j) {
+            load(it + j + DEPTH - 1, buf[(j + DEPTH - 1) % DEPTH]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (it + j < nsw) take_sweep(it + j, buf[j], it + j >= nfull);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
-    for (int v = nfull * SW + tid; v < nvec; v += THREADS) take(__builtin_nontemporal_load(vp + v));
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) acc ^= __shfl_xor(acc, off);
+    for (int t = 0; t < 6; ++t) {  // the wave's XOR on the exchange network, as the pass's reductions
+        uint32_t a, b;
+        trajspec::lane_pair(t, acc, a, b);
+        acc = a ^ b;
+    }
     if ((tid & 63) == 0) sink[((int64_t)blockIdx.x * (THREADS / 64) + (tid >> 6)) & 4095] = acc;
 }
 
