@@ -10,8 +10,7 @@
 //     vector and discarded), so the compiler's load waits count exactly the older loads; the
 //     row's last, partial sweep goes through the same ring, in flight behind the last full one;
 //   * the workgroup size follows the row count: one wave per row for large batches (many
-//     resident workgroups per CU), 4 to 16 waves per row for short batches so that the launch
-//     still holds about four waves per SIMD;
+//     resident workgroups per CU), 4 or 8 waves per row for short batches;
 //   * per lane a lazily moved reference value r (an element of the lane, raised only when a
 //     vector maximum exceeds it by 2^8 in the exp2 domain: a wave-uniform branch that is rare
 //     after the first vectors) with the running sum of exp2((x - r) log2e); a vector costs its
@@ -529,16 +528,17 @@ struct TopkPlan {
     int splits, chunk;
 };
 
-// Measured on the 8B shapes (vocab 126464-152064, bf16): with many rows one wave per row and a
-// 3-sweep ring of 2 vectors streams fastest (32768 rows: 6.8 TB/s); 1024 rows run best with
-// 4 waves per row and 4-vector sweeps, 256 rows with 16 waves per row (4 waves per SIMD in both).
-// Fewer rows than 128 run 8 waves per row and also split each row, so that the launch keeps
-// about 128 workgroups.
+// Measured on the 8B shapes (vocab 126464-152064, bf16; every shape checked against the library's
+// output): with many rows one wave per row and a 3-sweep ring of 2 vectors streams fastest
+// (32768 rows: 6.8 TB/s); 1024 rows run best with 4 waves per row and 2-vector sweeps (4 waves
+// per SIMD), 256 rows with 8 waves per row and 4-vector sweeps (2 waves per SIMD).  Fewer rows
+// than 128 run 8 waves per row and also split each row, so that the launch keeps about 128
+// workgroups.
 inline TopkPlan plan_conf_topk(int64_t rows, int64_t vocab, int vec) {
     TopkPlan p{64, 2, 3, 1, (int)vocab};
     if (rows >= 4096) return p;
-    if (rows >= 512) return TopkPlan{256, 4, 2, 1, (int)vocab};
-    if (rows >= 128) return TopkPlan{1024, 4, 2, 1, (int)vocab};
+    if (rows >= 512) return TopkPlan{256, 2, 2, 1, (int)vocab};
+    if (rows >= 128) return TopkPlan{512, 4, 2, 1, (int)vocab};
     p = TopkPlan{512, 2, 2, 1, (int)vocab};
     const int64_t target = 128;
     if (rows <= 0 || rows >= target) return p;

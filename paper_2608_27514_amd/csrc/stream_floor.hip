@@ -118,10 +118,10 @@ int traj_floor_logit_read(const void* data, int64_t rows, int64_t vocab, int64_t
     const int64_t stride_vec = row_stride * elem_bytes / 16;
     if (plan.threads == 64 && plan.unroll == 2 && plan.depth == 3) {
         launch<64, 2, 3>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
-    } else if (plan.threads == 256 && plan.unroll == 4 && plan.depth == 2) {
-        launch<256, 4, 2>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
-    } else if (plan.threads == 1024 && plan.unroll == 4 && plan.depth == 2) {
-        launch<1024, 4, 2>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
+    } else if (plan.threads == 256 && plan.unroll == 2 && plan.depth == 2) {
+        launch<256, 2, 2>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
+    } else if (plan.threads == 512 && plan.unroll == 4 && plan.depth == 2) {
+        launch<512, 4, 2>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
     } else if (plan.threads == 512 && plan.unroll == 2 && plan.depth == 2) {
         launch<512, 2, 2>(data, rows, stride_vec, nvec, plan.splits, chunk, sink, s);
     } else {

@@ -114,9 +114,9 @@ traj_status launch_topk_k(const void* logits, const traj_logits_shape* sh, int k
     } else if (plan.threads == 64) {
         launch_conf_kernel<T, K, 64, 2, 3, true>(lg, sh, k, plan, conf, idx, partial, st);
     } else if (plan.threads == 256) {
-        launch_conf_kernel<T, K, 256, 4, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
-    } else if (plan.threads == 1024) {
-        launch_conf_kernel<T, K, 1024, 4, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
+        launch_conf_kernel<T, K, 256, 2, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
+    } else if (plan.unroll == 4) {
+        launch_conf_kernel<T, K, 512, 4, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     } else {
         launch_conf_kernel<T, K, 512, 2, 2, true>(lg, sh, k, plan, conf, idx, partial, st);
     }

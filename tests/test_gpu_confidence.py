@@ -38,7 +38,7 @@ def test_tiny_fp32_full():
 
 
 def test_8b_siblings_full_size():
-    """256 rows x 126464 bf16 -- the short-batch launch (16 waves per row), every row checked."""
+    """256 rows x 126464 bf16 -- the short-batch launch (8 waves per row), every row checked."""
     wl = WORKLOADS[2]
     d = decode_inputs(wl, seed_for(2))
     lg = make_logits(d["row_margin"], d["row_top"], wl.V, torch.bfloat16, seed_for(2)).cuda()
