@@ -400,6 +400,46 @@ def logit_floor(copies, stream, reps):
             "us": ms * 1e3, "gbs": gbs, "frac_of_hbm": gbs / PEAK_HBM_GBS}
 
 
+def mfma_rate(x, stream, reps, flop_target):
+    """What the matrix cores sustain on the attention's own operand data: libtrajfloor's MFMA-rate
+    kernel (two 4-wave workgroups per CU, each wave issuing back-to-back 32x32x16 bf16 MFMAs on
+    fragments read from the cache K and the queries), sized to about the attention's FLOP per
+    launch and timed like it (graph_time).  The part holds a lower clock when the multiplies draw
+    more power, which depends on the operand bits; this is the ceiling of any kernel's MFMA rate
+    on such data, beside the nominal 2.5 PFLOP/s.  None when the library is not built."""
+    import ctypes
+    if not os.path.exists(FLOOR_LIB):
+        return None
+    lib = ctypes.CDLL(FLOOR_LIB)
+    fn = lib.traj_floor_mfma_rate
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    dev = x.q.device
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    grid = 2 * cus
+    per_iter = grid * 4 * 16 * 32768  # FLOP of one round: 16 MFMAs of 2 x 32 x 32 x 16 per wave, 4 waves per workgroup
+    iters = max(1, int(round(flop_target / per_iter)))
+    sink = torch.zeros(4096, dtype=torch.float32, device=dev)
+    clock = torch.zeros(2, dtype=torch.int64, device=dev)
+
+    def call(i, s):
+        r = fn(ctypes.c_void_p(x.kc.data_ptr()), x.kc.numel() * 2, ctypes.c_void_p(x.q.data_ptr()), x.q.numel() * 2,
+               grid, iters, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clock.data_ptr()),
+               ctypes.c_void_p(s.cuda_stream))
+        if r != 0:
+            raise RuntimeError("traj_floor_mfma_rate rejected its arguments")
+
+    ms = graph_time(call, stream, reps)
+    cyc, ticks = (int(v) for v in clock.cpu().tolist())
+    tflops = per_iter * iters / (ms * 1e-3) / 1e12
+    return {"kernel": "sustained MFMA rate (libtrajfloor): 32x32x16 bf16 MFMAs back to back on the attention's "
+                      "cache K / query data, two 4-wave workgroups per CU",
+            "flop_per_launch": per_iter * iters, "us": ms * 1e3, "tflops": tflops,
+            "frac_of_peak": tflops / PEAK_BF16_TFLOPS,
+            "clock_ghz": cyc / (ticks / 100e6) / 1e9 if ticks > 0 else None}
+
+
 def graph_time(launch, stream, reps, replays=5):
     """Per-launch ms of `reps` back-to-back launches (launch(i, s) enqueues the i-th on torch
     stream s), captured once in a HIP graph on a side stream and replayed between two HIP events
@@ -853,6 +893,12 @@ def main():
     floor = logit_floor(copies, stream, args.steps) if (args.with_floor or not args.no_extras) else None
     if floor is not None:
         floor["logit_pass_over_floor"] = t_conf * 1e3 / floor["us"]
+    sustained = None
+    if args.with_floor or not args.no_extras:
+        log("sustained MFMA rate on the attention's operands")
+        sustained = mfma_rate(copies[0], stream, args.steps, flops)
+        if sustained is not None:
+            sustained["attention_over_sustained"] = a_tflops / sustained["tflops"]
     status = tsp.device_status(reset=True)
 
     result = {
@@ -883,6 +929,7 @@ def main():
             "frac": a_tflops / PEAK_BF16_TFLOPS,
             "traffic": measured_traffic("verify_attn", wl.name),
             "algorithmic_flop_per_launch": flops,
+            "sustained_mfma": sustained,
         },
         "kernels_ms": {"verify_attn": t_attn, "confidence_topk": t_conf, "accept": t_acc},
         "logit_pass": {"bound": "hbm", "achieved": l_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -1,5 +1,6 @@
-// libtrajfloor: the streaming-read floor of the logit pass, a measurement aid (not part of the
-// verification step and not declared in the library's C ABI).
+// libtrajfloor: measurement aids (not part of the verification step and not declared in the
+// library's C ABI): the streaming-read floor of the logit pass, and the rate the matrix cores
+// sustain on the attention's own operand data.
 //
 // The kernel reads rows of bytes with exactly the launch shape and load pattern of the logit pass
 // (conf_topk.hpp): one workgroup per row, THREADS lanes, 16-byte non-temporal loads held in a ring
@@ -80,6 +81,63 @@ __global__ __launch_bounds__(THREADS) void stream_floor_kernel(const u32x4* __re
     if ((tid & 63) == 0) sink[((int64_t)blockIdx.x * (THREADS / 64) + (tid >> 6)) & 4095] = acc;
 }
 
+// The sustained bf16 MFMA rate: each wave loads four A and four B fragments (16 bytes per lane)
+// from the two operand arrays it is given (the attention's cache K and Q), then issues `iters`
+// rounds of 16 v_mfma_f32_32x32x16_bf16 on four independent accumulators -- the matrix cores'
+// own issue rate, with the data toggling as the attention's does (the power the multiplies draw,
+// and so the clock the part holds, depends on the operands).  Two 4-wave workgroups per CU, as
+// the attention.  Wave 0 of workgroup 0 records shader-clock cycles (s_memtime) and 100 MHz
+// reference ticks (s_memrealtime) around its loop.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint64_t shader_cycles() {
+    uint64_t t;
+    asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t)::"memory");
+    return t;
+}
+__device__ __forceinline__ uint64_t ref_ticks() {
+    uint64_t t;
+    asm volatile("s_memrealtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t)::"memory");
+    return t;
+}
+
+__global__ __launch_bounds__(256, 2) void mfma_rate_kernel(const u32x4* __restrict__ a_src, int64_t a_vecs,
+                                                           const u32x4* __restrict__ b_src, int64_t b_vecs, int iters,
+                                                           float* __restrict__ sink, uint64_t* __restrict__ clock) {
+    const int64_t gl = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    bf16x8 a[4], b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        a[i] = __builtin_bit_cast(bf16x8, a_src[(gl * 4 + i) % a_vecs]);
+        b[i] = __builtin_bit_cast(bf16x8, b_src[(gl * 4 + i) % b_vecs]);
+    }
+    f32x16 c[4] = {{}, {}, {}, {}};
+    uint64_t t0 = 0, r0 = 0;
+    const bool timer = blockIdx.x == 0 && threadIdx.x == 0;
+    if (timer) {
+        t0 = shader_cycles();
+        r0 = ref_ticks();
+    }
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                c[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(i + k) & 3], b[(3 * i + k) & 3], c[i], 0, 0, 0);
+    }
+    if (timer) {
+        clock[0] = shader_cycles() - t0;
+        clock[1] = ref_ticks() - r0;
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc += c[i][v];
+    if ((threadIdx.x & 63) == 0) sink[(gl >> 6) & 4095] = acc;  // keeps the products live
+}
+
 template <int THREADS, int U, int DEPTH>
 void launch(const void* data, int64_t rows, int64_t stride_vec, int nvec, int splits, int chunk, uint32_t* sink,
             hipStream_t s) {
@@ -127,6 +185,23 @@ int traj_floor_logit_read(const void* data, int64_t rows, int64_t vocab, int64_t
     } else {
         return -1;
     }
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// Sustained bf16 MFMA rate on operand data: grid workgroups of 256 threads (two per CU), each
+// wave running iters x 16 MFMAs of 32x32x16 (32768 FLOP each) on fragments read from a (a_bytes)
+// and b (b_bytes), both 16-byte aligned device arrays of at least 16 bytes.  sink: 4096 floats,
+// clock: 2 uint64 (device; shader cycles and 100 MHz ticks of wave 0 of workgroup 0).  Returns
+// 0, or -1 on bad arguments (nothing launched).
+int traj_floor_mfma_rate(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes, int32_t grid, int32_t iters,
+                         float* sink, uint64_t* clock, void* stream) {
+    if (a == nullptr || b == nullptr || sink == nullptr || clock == nullptr || a_bytes < 16 || b_bytes < 16 ||
+        grid < 1 || iters < 1)
+        return -1;
+    if (((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b)) & 15u) != 0) return -1;
+    hipLaunchKernelGGL(mfma_rate_kernel, dim3(grid), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                       static_cast<const u32x4*>(a), a_bytes / 16, static_cast<const u32x4*>(b), b_bytes / 16, iters,
+                       sink, clock);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
