@@ -499,6 +499,13 @@ def time_config(cid, stream, steps, warmup):
     kernels = time_kernels_apart(copies, buf, wl.tau, stream, steps)
     rec = step_record(wl, copies[0], ms_step, kernels, len(copies), steps)
     rec["kernel_us_in_step"] = {k: v * 1e3 for k, v in in_step.items()}
+    # the same step captured once as a HIP graph of `steps` back-to-back steps over the rotated
+    # copies and replayed (graph_time): what a serving loop that captures its step gets, without
+    # the host issue of three calls per step and the events around them
+    n = len(copies)
+    ms_graph = graph_time(lambda i, s: run_step(copies[i % n], buf, wl.tau, s), stream, steps)
+    rec["step_us_graph"] = ms_graph * 1e3
+    rec["tokens_per_s_graph"] = wl.B * wl.N * wl.L / (ms_graph * 1e-3)
     fl = logit_floor(copies, stream, steps)
     if fl is not None:
         fl["logit_pass_over_floor"] = kernels["confidence_topk"] * 1e3 / fl["us"]
