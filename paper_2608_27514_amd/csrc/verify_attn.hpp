@@ -517,6 +517,121 @@ __device__ __forceinline__ void full_step(int t, const CacheArgs& a, const AttnL
     __syncthreads();
 }
 
+// Ascending walk over the 32-key draft tiles that hold a block of `todo` (a wave-uniform set of
+// drafts): block j covers tiles (j L) / 32 .. (j L + L - 1) / 32, and a tile that an earlier
+// (lower) block already covered is not visited again.  cur .. hi are the current block's
+// remaining tiles; next() returns the next tile, or -1 once every block is done.
+struct TileWalk {
+    uint64_t todo;
+    int cur, hi;
+    __device__ __forceinline__ int next(int L) {
+        while (cur > hi) {
+            if (todo == 0ull) return -1;
+            const int jb = __builtin_ctzll(todo);
+            todo &= todo - 1ull;
+            cur = max((jb * L) >> 5, hi + 1);  // blocks ascend, so hi + 1 is the first tile not yet visited
+            hi = (jb * L + L - 1) >> 5;
+        }
+        return cur++;
+    }
+};
+
+// A wave-uniform 64-bit value moved to scalar registers (the compiler cannot see that the result of
+// a lane-exchange reduction is uniform).
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Orders a wave's LDS accesses around direct loads into its own region (no other wave touches it).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Per-wave constants of the draft phase.
+struct DraftArgs {
+    const uint16_t* kd;  // this K/V head's column of the packed draft keys / values
+    const uint16_t* vd;
+    int64_t seq_row0;    // b * N * L: first packed draft row of the sequence
+    int NL, N, L, kv_stride;
+    int wri, wpc;        // row and chunk slot of this lane within a wave-wide direct load
+    uint64_t anc;        // this lane's visible drafts (0 for rows past the workgroup's share)
+    bool row_valid;
+    int h;
+};
+
+template <int D>
+__device__ __forceinline__ DraftArgs draft_args(const AttnParams& P, int b, int g, int lane, uint64_t my_anc,
+                                                bool row_valid, int h) {
+    using G = AttnGeom<D>;
+    DraftArgs a;
+    a.kd = P.kd + (int64_t)g * D;
+    a.vd = P.vd + (int64_t)g * D;
+    a.NL = P.N * P.L;
+    a.seq_row0 = (int64_t)b * a.NL;
+    a.N = P.N;
+    a.L = P.L;
+    a.kv_stride = P.Hkv * D;
+    a.wri = lane / G::kChunks;
+    a.wpc = lane % G::kChunks;
+    a.anc = my_anc;
+    a.row_valid = row_valid;
+    a.h = h;
+    return a;
+}
+
+// Direct loads of the 32 draft keys k0 .. k0+31 into a wave's tile regions kw (K rows) and vw
+// (V rows), with the cache tiles' swizzles.  Rows past the packed drafts read the last draft key;
+// base and lane row are both clamped so the lane offset is never negative (those keys are masked).
+template <int D>
+__device__ __forceinline__ void draft_tile_dma(const DraftArgs& a, int k0, uint16_t* kw, uint16_t* vw) {
+    using G = AttnGeom<D>;
+#pragma unroll
+    for (int j = 0; j < G::kDraftDma; ++j) {
+        const int row0 = j * G::kRowsPerDma;
+        const int r = row0 + a.wri;
+        const int base_row = min(k0 + row0, a.NL - 1);
+        const int grow = min(k0 + r, a.NL - 1) - base_row;
+        const int64_t rowbase = (a.seq_row0 + base_row) * a.kv_stride;  // uniform
+        const unsigned ok = (unsigned)(grow * a.kv_stride + ((a.wpc ^ G::k_swz(r)) << 3));
+        const unsigned ov = (unsigned)(grow * a.kv_stride + ((a.wpc ^ G::v_rot(r)) << 3));
+        dma16(a.kd + rowbase + ok, kw + row0 * D);
+        dma16(a.vd + rowbase + ov, vw + row0 * D);
+    }
+}
+
+// Scores, weights and O += V P of the draft tile k0 .. k0+31 held in the wave's regions kw, vw.
+template <int D>
+__device__ __forceinline__ void draft_tile(const DraftArgs& a, int k0, const uint16_t* kw, const uint16_t* vw,
+                                           const AttnLane<D>& ln,
+                                           const bf16x8_t (&qf)[D / 16], SoftState& st, f32x16_t (&o)[D / 32],
+                                           float c, float thr) {
+    const int jlo = k0 / a.L;
+    const int jhi = min(a.N - 1, (k0 + 31) / a.L);
+    const uint64_t T = (jhi - jlo == 63) ? ~0ull : (((1ull << (jhi - jlo + 1)) - 1) << jlo);
+    const bool lane_full = !a.row_valid || ((a.anc & T) == T);
+    const bool all_full = ballot64_all(lane_full);
+    const bool full = (k0 + 32 <= a.NL) & all_full;
+    f32x16_t s = qk_block<D>(kw, ln.kq, qf);
+    if (!full) {
+        // branch-free per-element visibility (key beyond the packed drafts, or a block that is
+        // not on this row's root path)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int key = k0 + 8 * (v >> 2) + 4 * a.h + (v & 3);
+            const int blk = min(key, a.NL - 1) / a.L;
+            const bool vis = (key < a.NL) & (((a.anc >> blk) & 1ull) != 0ull);
+            s[v] = vis ? s[v] : kNegInf;
+        }
+    }
+    bf16x8_t pf[2];
+    softmax_update<D>(s, c, thr, st, o, pf);
+    pv_block<D>(vw, ln.vq, pf, o);
+}
+
 template <int D>
 __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams P) {
     using G = AttnGeom<D>;
@@ -703,71 +818,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void verify_attn_kernel(AttnParams
     int nd = 0;
     if (row_valid) (void)row_offset(nd);
     const uint64_t my_anc = row_valid ? anc[nd] : 0ull;
-    const uint64_t U = wave_or64(my_anc);
+    const DraftArgs da = draft_args<D>(P, b, g, lane, my_anc, row_valid, h);
+    // Visit the 32-key tiles that hold a block of any row's root path, in ascending order; each
+    // tile is loaded into the wave's region, then multiplied.
     uint16_t* kw = (wave < 2 ? buf0 : buf1) + (wave & 1) * G::kWaveRegionElems;
-    uint16_t* vw = kw + 32 * D;
-    const uint16_t* kd_base = P.kd + (int64_t)g * D;
-    const uint16_t* vd_base = P.vd + (int64_t)g * D;
-    const int wri = lane / G::kChunks;
-    const int wpc = lane % G::kChunks;
-    // Visit the 32-key tiles that hold a block of U (any row's root path), in ascending order:
-    // the blocks of U are taken lowest first and each covers tiles (j L) / 32 .. (j L + L - 1) / 32,
-    // skipping tiles an earlier block already covered.
-    uint64_t todo = U;  // wave-uniform
-    int next_tile = 0;
-    while (todo != 0ull) {
-      const int jb = __builtin_ctzll(todo);
-      todo &= todo - 1ull;
-      const int t_hi = (jb * L + L - 1) >> 5;
-      for (int tt = max((jb * L) >> 5, next_tile); tt <= t_hi; ++tt) {
-        const int k0 = tt * 32;
-        const int jlo = k0 / L;
-        const int jhi = min(N - 1, (k0 + 31) / L);
-        const uint64_t T = (jhi - jlo == 63) ? ~0ull : (((1ull << (jhi - jlo + 1)) - 1) << jlo);
-        const bool lane_full = !row_valid || ((my_anc & T) == T);
-        const bool all_full = ballot64_all(lane_full);
-        const bool full = (k0 + 32 <= NL) & all_full;
-        // load the 32 draft keys of this tile into the wave's own LDS region (rows past the
-        // packed drafts read the last draft key; they are masked)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-        for (int j = 0; j < G::kDraftDma; ++j) {
-            const int row0 = j * G::kRowsPerDma;
-            const int r = row0 + wri;
-            // rows past the packed drafts read the last draft key; base and lane row are both
-            // clamped so the lane offset is never negative
-            const int base_row = min(k0 + row0, NL - 1);
-            const int grow = min(k0 + r, NL - 1) - base_row;
-            const int64_t rowbase = ((int64_t)b * NL + base_row) * kv_stride;  // uniform
-            const unsigned ok = (unsigned)(grow * kv_stride + ((wpc ^ G::k_swz(r)) << 3));
-            const unsigned ov = (unsigned)(grow * kv_stride + ((wpc ^ G::v_rot(r)) << 3));
-            dma16(kd_base + rowbase + ok, kw + row0 * D);
-            dma16(vd_base + rowbase + ov, vw + row0 * D);
-        }
+    TileWalk walk{uniform64(wave_or64(my_anc)), 0, -1};
+    for (int tt = walk.next(L); tt >= 0; tt = walk.next(L)) {
+        wave_lds_sync();
+        draft_tile_dma<D>(da, tt * 32, kw, kw + 32 * D);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        f32x16_t s = qk_block<D>(kw, ln.kq, qf);
-        if (!full) {
-            // branch-free per-element visibility (key beyond the packed drafts, or a block
-            // that is not on this row's root path)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int key = k0 + 8 * (v >> 2) + 4 * h + (v & 3);
-                const int blk = min(key, NL - 1) / L;
-                const bool vis = (key < NL) & (((my_anc >> blk) & 1ull) != 0ull);
-                s[v] = vis ? s[v] : kNegInf;
-            }
-        }
-        bf16x8_t pf[2];
-        softmax_update<D>(s, c, thr, st, o, pf);
-        pv_block<D>(vw, ln.vq, pf, o);
-      }
-      next_tile = max(next_tile, t_hi + 1);
+        wave_lds_sync();
+        draft_tile<D>(da, tt * 32, kw, kw + 32 * D, ln, qf, st, o, c, thr);
     }
 
     // ---------------- epilogue ----------------
