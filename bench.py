@@ -39,7 +39,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 MALL_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {
-    "verify_attn": ("common.hpp", "verify_attn.hpp"),
+    "verify_attn": ("common.hpp", "verify_attn.hpp", "verify_attn16.hpp"),
     "confidence_topk": ("common.hpp", "conf_topk.hpp"),
 }
 

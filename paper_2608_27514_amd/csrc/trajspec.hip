@@ -17,6 +17,7 @@
 #include "layer.hpp"
 #include "tree.hpp"
 #include "verify_attn.hpp"
+#include "verify_attn16.hpp"
 
 // Fixed device scratch of traj_confidence_topk_noalloc: the split records of short batches
 // (at most TRAJ_TOPK_SCRATCH_BYTES).  Host code must not pass this name to a kernel or a copy: on
@@ -67,9 +68,30 @@ traj_status check_attn(const traj_attn_shape* sh) {
     return TRAJ_OK;
 }
 
+// Compute units of the current device (0 when the query fails).
+int device_cu_count() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    return cus;
+}
+
+// p describes the 32-row launch (4 waves x 32 rows per workgroup).  A grid that still has at
+// most one workgroup per CU with 16-row waves (4 waves x 16 rows per workgroup, twice the
+// workgroups) runs that way: each wave's chain of steps is half as long.  Larger grids keep
+// 32-row waves: with two 16-row workgroups per CU the doubled LDS fragment reads and stage loads
+// per MFMA cost more than the second wave per SIMD gains.
 template <int D>
-traj_status launch_attn(const AttnParams& p, hipStream_t st) {
-    hipLaunchKernelGGL(verify_attn_kernel<D>, dim3(p.num_wg), dim3(kAttnThreads), 0, st, p);
+traj_status launch_attn(AttnParams p, hipStream_t st) {
+    const int wg16 = (p.rows_per_group + kAttnWaves * 16 - 1) / (kAttnWaves * 16);
+    const int64_t nwg16 = (int64_t)p.B * p.Hkv * wg16;
+    if (nwg16 <= device_cu_count()) {
+        p.wg_per_group = wg16;
+        p.num_wg = (int)nwg16;
+        hipLaunchKernelGGL(verify_attn16_kernel<D>, dim3(p.num_wg), dim3(kAttnThreads), 0, st, p);
+    } else {
+        hipLaunchKernelGGL(verify_attn_kernel<D>, dim3(p.num_wg), dim3(kAttnThreads), 0, st, p);
+    }
     return launched();
 }
 

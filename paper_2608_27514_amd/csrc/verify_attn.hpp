@@ -86,7 +86,10 @@ constexpr float kLazyLog2 = 8.0f;
 
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 
-template <int D>
+// R = query rows per wave (32: v_mfma_f32_32x32x16_bf16; 16: v_mfma_f32_16x16x32_bf16).  Only the
+// V tile's chunk swizzle depends on it: it is chosen so that the rows one half-wave reads with a
+// transposing load fall into distinct bank groups.
+template <int D, int R = 32>
 struct AttnGeom {
     static constexpr int kChunks = D / 8;                         // 16-byte chunks per row
     static constexpr int kTileElems = kAttnTile * D;              // one K or V tile
@@ -99,6 +102,7 @@ struct AttnGeom {
 
     static __device__ __forceinline__ int k_swz(int r) { return kChunks == 16 ? (r & 15) : ((r >> 1) & 7); }
     static __device__ __forceinline__ int v_rot(int r) {
+        if (R == 16) return kChunks == 16 ? ((r & 7) << 1) : (((r >> 1) & 3) << 1);
         return kChunks == 16 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
     }
 };
@@ -286,10 +290,10 @@ struct AttnLane {
 // a scalar base plus this lane's 32-bit offset.  RAGGED clamps keys >= S to key S-1 (their
 // scores are masked or never computed; the clamped values stay finite); the uniform base row
 // is clamped too, so a lane's offset from it is never negative.
-template <int D, bool RAGGED, bool IS_V>
+template <int D, bool RAGGED, bool IS_V, int R = 32, typename LaneT>
 __device__ __forceinline__ void cache_rows_dma(__amdgpu_buffer_rsrc_t rs, int kv_stride, int key0, int S, int wave,
-                                               const AttnLane<D>& ln, uint16_t* dst) {
-    using G = AttnGeom<D>;
+                                               const LaneT& ln, uint16_t* dst) {
+    using G = AttnGeom<D, R>;
 #pragma unroll
     for (int j = 0; j < G::kDmaPerWave; ++j) {
         const int row0 = wave * (kAttnTile / kAttnWaves) + j * G::kRowsPerDma;  // uniform
@@ -311,12 +315,12 @@ __device__ __forceinline__ void cache_rows_dma(__amdgpu_buffer_rsrc_t rs, int kv
 // the K rows of keys 64 t + 64 .. 64 t + 127 (blocks 2t+2, 2t+3): the matrix phase of step t
 // multiplies the V rows of the blocks whose weights were just computed and the K rows of the
 // next two blocks, so one buffer and one barrier per stage suffice.  RAGGED when 64 t + 128 > S.
-template <int D, bool RAGGED>
+template <int D, bool RAGGED, int R = 32, typename LaneT>
 __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t vrs, int kv_stride, int t,
-                                          int S, int wave, const AttnLane<D>& ln, uint16_t* stage) {
-    using G = AttnGeom<D>;
-    cache_rows_dma<D, RAGGED, false>(krs, kv_stride, t * kAttnTile + kAttnTile, S, wave, ln, stage);
-    cache_rows_dma<D, RAGGED, true>(vrs, kv_stride, t * kAttnTile, S, wave, ln, stage + G::kTileElems);
+                                          int S, int wave, const LaneT& ln, uint16_t* stage) {
+    using G = AttnGeom<D, R>;
+    cache_rows_dma<D, RAGGED, false, R>(krs, kv_stride, t * kAttnTile + kAttnTile, S, wave, ln, stage);
+    cache_rows_dma<D, RAGGED, true, R>(vrs, kv_stride, t * kAttnTile, S, wave, ln, stage + G::kTileElems);
 }
 
 // Softmax phase of a 64-key step: the weights of two blocks (s[0], s[1]) against the query's
@@ -586,9 +590,9 @@ __device__ __forceinline__ DraftArgs draft_args(const AttnParams& P, int b, int 
 // Direct loads of the 32 draft keys k0 .. k0+31 into a wave's tile regions kw (K rows) and vw
 // (V rows), with the cache tiles' swizzles.  Rows past the packed drafts read the last draft key;
 // base and lane row are both clamped so the lane offset is never negative (those keys are masked).
-template <int D>
+template <int D, int R = 32>
 __device__ __forceinline__ void draft_tile_dma(const DraftArgs& a, int k0, uint16_t* kw, uint16_t* vw) {
-    using G = AttnGeom<D>;
+    using G = AttnGeom<D, R>;
 #pragma unroll
     for (int j = 0; j < G::kDraftDma; ++j) {
         const int row0 = j * G::kRowsPerDma;

@@ -52,6 +52,36 @@ def _check(out, inputs, parent, variant, scale=None):
     return attn_close(out, ref, aw)
 
 
+def _cus():
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+def _wg16(wl):
+    """Workgroups per (sequence, K/V head) with 16-row waves (4 waves x 16 rows each)."""
+    return -(-((wl.Hq // wl.Hkv) * wl.N * wl.L) // 64)
+
+
+def _tiling_batch(wl, tiling):
+    """The batch that makes the library launch the given row tiling: one-sequence-sized grids
+    (16-row grid at most one workgroup per CU) run with 16-row waves, larger ones with 32-row
+    waves.  '16' keeps wl.B (asserting that it is in that regime); '32' takes the smallest batch
+    past the threshold."""
+    if tiling == "16":
+        assert wl.B * wl.Hkv * _wg16(wl) <= _cus(), "shape is not in the 16-row regime"
+        return wl.B
+    return _cus() // (wl.Hkv * _wg16(wl)) + 1
+
+
+def _check_seqs(out, inputs, parent, variant, seqs):
+    """Oracle check of the sequences `seqs` only (sequences are independent)."""
+    for b in seqs:
+        sub = [t[b:b + 1] for t in inputs]
+        ok, worst, frac = _check(out[b:b + 1], sub, parent[b:b + 1], variant)
+        if not ok:
+            return False, worst, frac, b
+    return True, 0.0, 0.0, None
+
+
 SMALL = {
     # name: workload (reduced heads where the full one would be slow for the oracle)
     "tiny": WORKLOADS[1],
@@ -87,6 +117,7 @@ def test_wrong_mask_is_detected(name):
     assert not ok
 
 
+@pytest.mark.parametrize("tiling", ["16", "32"])
 @pytest.mark.parametrize("L,N,S,Hq,Hkv,D", [
     (8, 4, 192, 4, 4, 64),      # rows of one wave span 4 drafts
     (40, 5, 70, 2, 1, 128),     # L not a multiple of 32, ragged cache tile
@@ -97,18 +128,23 @@ def test_wrong_mask_is_detected(name):
     (64, 64, 100, 2, 1, 128),   # both maxima: 64 drafts of 64 tokens, a 64-deep chain
     (5, 1, 1, 1, 1, 128),       # single draft, single cache key
 ])
-def test_odd_shapes(L, N, S, Hq, Hkv, D):
+def test_odd_shapes(L, N, S, Hq, Hkv, D, tiling):
+    """Edge shapes under both row tilings of the kernel (16 query rows per wave on one-sequence
+    grids, 32 on larger ones: the batch is chosen to fall on either side of the threshold; with
+    the larger batch the first and last sequences are checked)."""
     wl = Workload(99, "odd", B=2, N=N, L=L, Hq=Hq, Hkv=Hkv, D=D, S_prefix=S, S_suffix=0, V=64,
                   logits_dtype="f32", margin_max=3.0, parents=None, level_sizes=None)
+    B = _tiling_batch(wl, tiling)
+    wl = wl.with_(B=B)
     rng = np.random.default_rng(L * 1000 + N)
-    parent = np.array([[-1] + [int(rng.integers(-1, n)) for n in range(1, N)] for _ in range(2)],
+    parent = np.array([[-1] + [int(rng.integers(-1, n)) for n in range(1, N)] for _ in range(B)],
                       dtype=np.int32)
     if N == 64:
         parent[0] = np.arange(-1, N - 1)
     for variant in ("spec", "sharp"):
         inputs, _, out = _run(wl, 7 + L, variant, parent=parent)
-        ok, worst, frac = _check(out, inputs, parent, variant)
-        assert ok, f"{variant}: worst excess {worst:.3g}, {frac:.2%} bad"
+        ok, worst, frac, b = _check_seqs(out, inputs, parent, variant, sorted({0, B - 1}))
+        assert ok, f"{variant} B={B} b={b}: worst excess {worst:.3g}, {frac:.2%} bad"
 
 
 def test_explicit_scale():
@@ -224,28 +260,34 @@ def test_bad_shapes_raise():
                         kd[..., :48].contiguous(), vd[..., :48].contiguous(), par)
 
 
+@pytest.mark.parametrize("tiling", ["16", "32"])
 @pytest.mark.parametrize("S", [1, 63, 64, 65, 127, 128, 129, 191, 192, 193, 255, 256, 257, 320, 383, 384, 449])
-def test_cache_lengths_cover_every_tail_path(S):
+def test_cache_lengths_cover_every_tail_path(S, tiling):
     """The cache loop runs full tiles in pairs and peels 0-2 full tiles plus a last
-    (ragged or full) tile: every cache length class in 64-key tiles must agree."""
+    (ragged or full) tile: every cache length class in 64-key tiles must agree, under both row
+    tilings."""
     wl = Workload(98, "cache-len", B=1, N=3, L=32, Hq=2, Hkv=1, D=128, S_prefix=S, S_suffix=0, V=64,
                   logits_dtype="f32", margin_max=3.0, parents=(-1, 0, 0), level_sizes=None)
-    parent = np.array([[-1, 0, 0]], dtype=np.int32)
+    B = _tiling_batch(wl, tiling)
+    wl = wl.with_(B=B)
+    parent = np.tile(np.array([[-1, 0, 0]], dtype=np.int32), (B, 1))
     for variant in ("spec", "sharp"):
         inputs, _, out = _run(wl, 1000 + S, variant, parent=parent)
-        ok, worst, frac = _check(out, inputs, parent, variant)
-        assert ok, f"S={S} {variant}: worst excess {worst:.3g}, {frac:.2%} bad"
+        ok, worst, frac, b = _check_seqs(out, inputs, parent, variant, sorted({0, B - 1}))
+        assert ok, f"S={S} {variant} B={B} b={b}: worst excess {worst:.3g}, {frac:.2%} bad"
 
 
+@pytest.mark.parametrize("tiling", ["16", "32"])
 @pytest.mark.parametrize("where", ["block0", "main_loop", "tail_stage", "partial_block", "ancestor_draft", "own_draft"])
-def test_reference_moves_late(where):
+def test_reference_moves_late(where, tiling):
     """Keys whose scores jump far above every earlier block (about 25 powers of two on the
     sharp inputs) force the lazy reference to move and O and the running sum to be rescaled at
     that point: in the first block, inside the paired stage loop, in the tail stages, in the
     partial last block, or in the draft phase.  The result must still match the oracle."""
     wl = Workload(97, "jump", B=1, N=4, L=32, Hq=2, Hkv=1, D=128, S_prefix=700, S_suffix=0, V=64,
                   logits_dtype="f32", margin_max=3.0, parents=(-1, 0, 1, 1), level_sizes=None)
-    parent = np.array([[-1, 0, 1, 1]], dtype=np.int32)
+    wl = wl.with_(B=_tiling_batch(wl, tiling))
+    parent = np.tile(np.array([[-1, 0, 1, 1]], dtype=np.int32), (wl.B, 1))
     q, kc, vc, kd, vd = attention_inputs(wl, 4242, "sharp")
     # 700 keys = 22 blocks of 32: blocks 0-15 run in the paired stage loop, 16-21 in the tail
     # stages, block 21 is partial (keys 672-699)
@@ -260,5 +302,5 @@ def test_reference_moves_late(where):
     inputs = (q, kc, vc, kd, vd)
     out = tsp.verify_attn(*[x.cuda() for x in inputs], cuda(parent, torch.int32))
     torch.cuda.synchronize()
-    ok, worst, frac = _check(out, inputs, parent, "sharp")
+    ok, worst, frac, _ = _check_seqs(out, inputs, parent, "sharp", [0])  # the jump is in sequence 0
     assert ok, f"{where}: worst excess {worst:.3g}, {frac:.2%} outside tolerance"

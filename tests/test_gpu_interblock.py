@@ -31,18 +31,32 @@ def _peers_tensor(rows):
     return torch.from_numpy(arr.view(np.int64).copy()).cuda()
 
 
-def _run(wl, parent, peers_rows, variant, seed):
+def _run(wl, parent, peers_rows, variant, seed, seqs=None):
+    """GPU output of the sequences `seqs` (default: all) with the oracle's reference for them."""
     inputs = attention_inputs(wl, seed, variant)
     args = [t.cuda() for t in inputs]
     out = tsp.verify_attn(*args, cuda(parent, torch.int32), peers=_peers_tensor(peers_rows))
     torch.cuda.synchronize()
-    x = [np64(t) for t in inputs]
-    ref = oracle.verify_attention(*x, parent, peers=peers_rows)
+    seqs = list(range(wl.B)) if seqs is None else list(seqs)
+    x = [np64(t)[seqs] for t in inputs]
+    par = parent[seqs]
+    peers = [peers_rows[b] for b in seqs]
+    ref = oracle.verify_attention(*x, par, peers=peers)
     aw = None
     if variant == "sharp":
         q, kc, vc, kd, vd = x
-        aw = oracle.verify_attention(q, kc, np.abs(vc), kd, np.abs(vd), parent, peers=peers_rows)
-    return out, ref, aw
+        aw = oracle.verify_attention(q, kc, np.abs(vc), kd, np.abs(vd), par, peers=peers)
+    return out[seqs], ref, aw
+
+
+def _batch_for_tiling(N, L, Hq, Hkv, tiling):
+    """2 sequences (a one-sequence-sized grid: 16 query rows per wave), or the smallest batch
+    whose grid of 16-row workgroups (4 waves x 16 rows) exceeds the CU count, which the library
+    runs with 32-row waves."""
+    if tiling == "16":
+        return 2
+    wg16 = -(-((Hq // Hkv) * N * L) // 64)
+    return torch.cuda.get_device_properties(0).multi_processor_count // (Hkv * wg16) + 1
 
 
 @pytest.mark.parametrize("L,N,S,Hq,Hkv,D", [
@@ -52,9 +66,10 @@ def _run(wl, parent, peers_rows, variant, seed):
     (8, 9, 33, 2, 1, 128),      # several drafts per 32-key tile
 ])
 @pytest.mark.parametrize("variant", ["spec", "sharp"])
-def test_peers_parity(L, N, S, Hq, Hkv, D, variant):
+@pytest.mark.parametrize("tiling", ["16", "32"])
+def test_peers_parity(L, N, S, Hq, Hkv, D, variant, tiling):
     rng = np.random.default_rng(L * 100 + N)
-    B = 2
+    B = _batch_for_tiling(N, L, Hq, Hkv, tiling)
     wl = _wl(B, N, L, Hq, Hkv, D, S)
     if N == 11:
         parent = np.array([[-1, 0, 0, 0, 1, 2, 4, -1, 7, 8, 9]] * B, dtype=np.int32)
@@ -63,7 +78,7 @@ def test_peers_parity(L, N, S, Hq, Hkv, D, variant):
         parent = np.array([[-1] + [int(rng.integers(-1, n)) for n in range(1, N)] for _ in range(B)], dtype=np.int32)
         peers_rows = [[int(rng.integers(0, 1 << 62)) | (int(rng.integers(0, 2)) << 63) for _ in range(N)]
                       for _ in range(B)]
-    out, ref, aw = _run(wl, parent, peers_rows, variant, seed=N + L)
+    out, ref, aw = _run(wl, parent, peers_rows, variant, seed=N + L, seqs=sorted({0, B - 1}))
     ok, worst, frac = attn_close(out, ref, aw)
     assert ok, f"{variant}: worst excess {worst:.3g}, {frac:.2%} outside tolerance"
 
